@@ -1,0 +1,165 @@
+/*
+ * adaspa.h - C ABI of the AdaSpa attention hot path for AMD MI355X (gfx950).
+ *
+ * AdaSpa (arXiv 2502.21079) accelerates the 3D full attention of video
+ * diffusion transformers with blockified sparse attention whose block pattern
+ * is found by a precise online search that reuses log-sum-exp values across
+ * denoising steps.  This library exposes the three operations of that path:
+ *
+ *   adaspa_dense_attn_lse     dense softmax attention + per-row LSE
+ *                             (Sec. 2.2; first pass of Algorithm 1)
+ *   adaspa_block_search       block attention mass W_sum_attn from a given
+ *                             LSE (second pass of Algorithm 1 / Algorithm 2,
+ *                             Sec. 4.1-4.2) and per-head block selection
+ *                             (optimal sparse indices of Sec. 4.1, text sink
+ *                             and row-wise uniform selection of Sec. 4.3)
+ *   adaspa_block_sparse_attn  blockified sparse attention over the selected
+ *                             key blocks (Sec. 4.1, bias form with c -> inf)
+ *
+ * Conventions shared by every call
+ * --------------------------------
+ *  - Tensors are DEVICE pointers, contiguous, 16-byte aligned.
+ *    Q, K, V, O: bf16 [B, H, L, D] (D innermost).  LSE: fp32 [B, H, L],
+ *    natural logarithm.  W_sum_attn: fp32 [B, H, NB, NB] with NB = ceil(L/Bs).
+ *  - Block rows of the sparse pattern are numbered r = (b*H + h)*NB + p for
+ *    query block p; the pattern is CSR: row_ptr int32 [B*H*NB + 1] and col_idx
+ *    int32, key-block indices strictly ascending within a row.
+ *  - A block is a TEXT block when its token range overlaps
+ *    [text_start, text_start + text_len).
+ *  - Ownership: the caller owns every buffer.  No call allocates device
+ *    memory, keeps a pointer after it returns, or synchronises the device:
+ *    each call validates its arguments on the host, enqueues kernels on
+ *    `stream` (a hipStream_t; NULL means the default stream) and returns.
+ *  - Errors: invalid arguments are reported synchronously with a status code
+ *    before anything is enqueued.  A failed launch returns ADASPA_ERR_HIP.
+ *    A fault inside a kernel surfaces at the caller's next synchronisation.
+ *  - Calls are stateless and may be issued from several host threads on
+ *    different streams; calls that share an output buffer must be ordered by
+ *    the caller.
+ */
+#ifndef ADASPA_H_
+#define ADASPA_H_
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  ADASPA_OK = 0,
+  ADASPA_ERR_INVALID_ARG = 1,   /* null/misaligned pointer, bad size or range */
+  ADASPA_ERR_UNSUPPORTED = 2,   /* head_dim or block outside what is built    */
+  ADASPA_ERR_CAPACITY = 3,      /* col_idx capacity too small                 */
+  ADASPA_ERR_WORKSPACE = 4,     /* workspace missing or too small             */
+  ADASPA_ERR_HIP = 5            /* a HIP launch reported an error             */
+} adaspa_status;
+
+/* Shape of one attention call: B batches x H heads of L tokens with head
+ * dimension D; square sparse blocks of Bs tokens.  Supported: D in {64, 128},
+ * Bs in {64, 128}, L >= 1 (L need not be a multiple of Bs: the last block is
+ * ragged and out-of-range keys never contribute).  softmax_scale <= 0 selects
+ * 1/sqrt(D) (the attention-weights equation, Sec. 2.2). */
+typedef struct {
+  int32_t batch, heads, seqlen, head_dim;
+  int32_t block;
+  int32_t text_start, text_len;   /* text range for the text sink; len may be 0 */
+  float softmax_scale;
+} adaspa_problem;
+
+/* Selection modes (Sec. 4.1 optimal sparse indices; Sec. 4.2 head-adaptive
+ * sparsity; Sec. 4.3 row-wise uniform selection).  In every mode each video
+ * query-block row of head h keeps the same count k_h of key blocks: text key
+ * blocks first (text sink), then the remaining blocks by mass descending with
+ * ties to the lower index.  Text query-block rows keep all NB blocks. */
+enum {
+  /* k_h = clamp(ceil(head_param_bp[h] * NB / 10000), max(1, #text blocks), NB) */
+  ADASPA_SELECT_TOPK = 0,
+  /* k_h = smallest count whose head Recall (Sec. 2.3, text rows counted as
+   * fully kept) reaches head_param_bp[h] / 10000. */
+  ADASPA_SELECT_COVERAGE = 1
+};
+
+/* Flags */
+enum {
+  ADASPA_F_TEXT_SINK = 1,       /* force text blocks (Sec. 4.3); usually set   */
+  ADASPA_F_SCORES_GIVEN = 2     /* block_mass is an INPUT: skip the mass pass  */
+};
+
+typedef struct {
+  int32_t mode;                 /* ADASPA_SELECT_*                                */
+  int32_t flags;                /* ADASPA_F_*                                     */
+  const int32_t* head_param_bp; /* HOST array [H]: keep fraction (TOPK) or Recall
+                                   target (COVERAGE) in basis points, 0..10000;
+                                   applies to every batch element               */
+} adaspa_select;
+
+/* Human-readable name of a status code (static storage). */
+const char* adaspa_status_string(adaspa_status s);
+
+/* Dense attention with LSE (Sec. 2.2; Algorithm 1, first pass).
+ *   out[b,h,i,:] = sum_j softmax_j(scale * q_i . k_j) v_j        bf16 (RNE)
+ *   lse[b,h,i]   = log sum_j exp(scale * q_i . k_j)             fp32
+ * q, k, v, out: bf16 [B,H,L,D]; lse: fp32 [B,H,L] (may be NULL to skip). */
+adaspa_status adaspa_dense_attn_lse(const adaspa_problem* prob, const void* q,
+                                    const void* k, const void* v, void* out,
+                                    float* lse, void* stream);
+
+/* Device bytes of workspace adaspa_block_search needs for this problem and
+ * selection (0 for invalid arguments). */
+size_t adaspa_block_search_workspace(const adaspa_problem* prob,
+                                     const adaspa_select* sel);
+
+/* Number of col_idx entries the selection may write: the exact count for
+ * TOPK, B*H*NB*NB for COVERAGE (the count depends on the data and the library
+ * never synchronises to learn it).  Returns -1 for invalid arguments. */
+int64_t adaspa_block_search_capacity(const adaspa_problem* prob,
+                                     const adaspa_select* sel);
+
+/* Block search (Sec. 4.1-4.3; Algorithm 1 second pass / Algorithm 2).
+ *   1. Unless ADASPA_F_SCORES_GIVEN: block_mass[b,h,p,c] =
+ *        sum_{i in block p} sum_{j in block c} exp(scale * q_i . k_j - lse[b,h,i])
+ *      with the LSE given by the caller (fresh from adaspa_dense_attn_lse, or
+ *      cached from an earlier step); no renormalisation.
+ *   2. Per-head count k_h (see the modes) and per-row selection, emitted as CSR
+ *      into row_ptr / col_idx.  head_k int32 [B,H] and head_recall fp32 [B,H]
+ *      (the head Recall at k_h) are optional outputs (may be NULL).
+ * Ranking compares fp32 masses (-0 == +0, NaN last).  Cumulative masses are
+ * exact: each mass m >= 0 becomes min(round_half_even(m * 2^32), cap) with
+ * cap = floor(2^62 / (NB*NB)) (NaN and m <= 0 give 0); coverage holds when
+ * kept * 10000 >= total * tau_bp; recall = (float)((double)kept/(double)total),
+ * 1 when total is 0.
+ * q, k, lse may be NULL with ADASPA_F_SCORES_GIVEN.  col_capacity must be at
+ * least adaspa_block_search_capacity(); workspace must hold
+ * adaspa_block_search_workspace() bytes, 256-byte aligned. */
+adaspa_status adaspa_block_search(const adaspa_problem* prob, const void* q,
+                                  const void* k, const float* lse,
+                                  const adaspa_select* sel, float* block_mass,
+                                  int32_t* row_ptr, int32_t* col_idx,
+                                  int64_t col_capacity, int32_t* head_k,
+                                  float* head_recall, void* workspace,
+                                  size_t workspace_bytes, void* stream);
+
+/* Blockified sparse attention (Sec. 4.1, bias -c(1-M) with c -> inf).
+ *   out[b,h,i,:] = sum_{j in kept(p(i))} exp(scale*q_i.k_j - lseM_i) v_j
+ *   lseM[b,h,i]  = log sum_{j in kept(p(i))} exp(scale * q_i . k_j)
+ * where kept(p) are the key blocks col_idx[row_ptr[r] .. row_ptr[r+1]) of
+ * row r = (b*H+h)*NB + p.  A row that keeps nothing gives out = 0 and
+ * lseM = -inf.  Keeping every block reproduces adaspa_dense_attn_lse bit for
+ * bit (both run the same main loop).  lse_out may be NULL.  col_count is
+ * the number of readable col_idx entries: row bounds are clamped to
+ * [0, col_count] and entries outside [0, NB) are skipped, so malformed
+ * patterns never read out of bounds.  Rows should be strictly ascending
+ * (a repeated block would be counted twice). */
+adaspa_status adaspa_block_sparse_attn(const adaspa_problem* prob, const void* q,
+                                       const void* k, const void* v,
+                                       const int32_t* row_ptr,
+                                       const int32_t* col_idx, int64_t col_count,
+                                       void* out, float* lse_out, void* stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* ADASPA_H_ */

@@ -1,0 +1,249 @@
+"""Python binding of libadaspa, the MI355X (gfx950) AdaSpa attention hot path.
+
+Argument marshalling only: every step runs in the HIP kernels of
+``libadaspa.so``.  PyTorch provides device memory and the current stream.
+The three calls mirror the C ABI in ``include/adaspa.h``:
+
+* :func:`dense_attn_lse`     dense attention + LSE (Sec. 2.2; Algorithm 1 pass 1)
+* :func:`block_search`       block masses from a given LSE (Algorithm 1 pass 2 /
+                             Algorithm 2) and per-head block selection
+                             (Sec. 4.1 optimal indices, Sec. 4.3 text sink and
+                             row-wise uniform selection)
+* :func:`block_sparse_attn`  blockified sparse attention (Sec. 4.1)
+
+There is no CPU fallback: if the library is missing, every call raises.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from dataclasses import dataclass
+from typing import Optional, Sequence
+
+import torch
+
+__all__ = ["dense_attn_lse", "block_search", "block_sparse_attn", "SearchResult",
+           "library_path", "load_library", "AdaspaError", "EXPORTED_SYMBOLS",
+           "block_search_workspace", "block_search_capacity"]
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_LIB_NAME = "libadaspa.so"
+
+EXPORTED_SYMBOLS = ("adaspa_status_string", "adaspa_dense_attn_lse",
+                    "adaspa_block_search_workspace", "adaspa_block_search_capacity",
+                    "adaspa_block_search", "adaspa_block_sparse_attn")
+
+SELECT_TOPK = 0
+SELECT_COVERAGE = 1
+F_TEXT_SINK = 1
+F_SCORES_GIVEN = 2
+
+
+class AdaspaError(RuntimeError):
+    pass
+
+
+class _Problem(ctypes.Structure):
+    _fields_ = [("batch", ctypes.c_int32), ("heads", ctypes.c_int32),
+                ("seqlen", ctypes.c_int32), ("head_dim", ctypes.c_int32),
+                ("block", ctypes.c_int32), ("text_start", ctypes.c_int32),
+                ("text_len", ctypes.c_int32), ("softmax_scale", ctypes.c_float)]
+
+
+class _Select(ctypes.Structure):
+    _fields_ = [("mode", ctypes.c_int32), ("flags", ctypes.c_int32),
+                ("head_param_bp", ctypes.POINTER(ctypes.c_int32))]
+
+
+_lib = None
+
+
+def library_path() -> str:
+    return os.environ.get("ADASPA_LIB", os.path.join(_HERE, _LIB_NAME))
+
+
+def load_library():
+    """Load libadaspa.so (once).  Raises if it is missing: there is no fallback."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    path = library_path()
+    if not os.path.exists(path):
+        raise AdaspaError(f"{path} not found; build it with "
+                          f"`python -m paper_2502_21079_amd.build`")
+    lib = ctypes.CDLL(path)
+    P, S = ctypes.POINTER(_Problem), ctypes.POINTER(_Select)
+    vp, i32p, f32p = ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p
+    lib.adaspa_status_string.restype = ctypes.c_char_p
+    lib.adaspa_status_string.argtypes = [ctypes.c_int]
+    lib.adaspa_dense_attn_lse.restype = ctypes.c_int
+    lib.adaspa_dense_attn_lse.argtypes = [P, vp, vp, vp, vp, f32p, vp]
+    lib.adaspa_block_search_workspace.restype = ctypes.c_size_t
+    lib.adaspa_block_search_workspace.argtypes = [P, S]
+    lib.adaspa_block_search_capacity.restype = ctypes.c_int64
+    lib.adaspa_block_search_capacity.argtypes = [P, S]
+    lib.adaspa_block_search.restype = ctypes.c_int
+    lib.adaspa_block_search.argtypes = [P, vp, vp, f32p, S, f32p, i32p, i32p, ctypes.c_int64,
+                                        i32p, f32p, vp, ctypes.c_size_t, vp]
+    lib.adaspa_block_sparse_attn.restype = ctypes.c_int
+    lib.adaspa_block_sparse_attn.argtypes = [P, vp, vp, vp, i32p, i32p, ctypes.c_int64, vp,
+                                             f32p, vp]
+    _lib = lib
+    return lib
+
+
+def _check(status: int):
+    if status != 0:
+        msg = load_library().adaspa_status_string(status).decode()
+        raise AdaspaError(f"libadaspa status {status}: {msg}")
+
+
+def _ptr(t: Optional[torch.Tensor]):
+    return None if t is None else ctypes.c_void_p(t.data_ptr())
+
+
+def _stream(device) -> ctypes.c_void_p:
+    return ctypes.c_void_p(torch.cuda.current_stream(device).cuda_stream)
+
+
+def _problem(q: torch.Tensor, block: int, text_start: int, text_len: int,
+             scale: Optional[float]) -> _Problem:
+    B, H, L, D = q.shape
+    return _Problem(B, H, L, D, block, text_start, text_len,
+                    0.0 if scale is None else float(scale))
+
+
+def _check_qkv(*ts):
+    ref = ts[0]
+    for t in ts:
+        if t is None:
+            continue
+        if t.dtype != torch.bfloat16 or t.device.type != "cuda" or not t.is_contiguous():
+            raise AdaspaError("q, k, v must be contiguous bf16 CUDA tensors [B, H, L, D]")
+        if t.shape != ref.shape:
+            raise AdaspaError(f"shape mismatch {tuple(t.shape)} vs {tuple(ref.shape)}")
+
+
+def _select(mode: str, head_param_bp: Sequence[int], text_sink: bool, scores_given: bool):
+    m = {"topk": SELECT_TOPK, "coverage": SELECT_COVERAGE}[mode]
+    arr = (ctypes.c_int32 * len(head_param_bp))(*[int(x) for x in head_param_bp])
+    flags = (F_TEXT_SINK if text_sink else 0) | (F_SCORES_GIVEN if scores_given else 0)
+    return _Select(m, flags, ctypes.cast(arr, ctypes.POINTER(ctypes.c_int32))), arr
+
+
+def dense_attn_lse(q, k, v, *, scale: Optional[float] = None, out=None, lse=None,
+                   want_lse: bool = True):
+    """Dense attention and per-row natural-log LSE.  Returns (out, lse)."""
+    _check_qkv(q, k, v)
+    lib = load_library()
+    B, H, L, D = q.shape
+    if out is None:
+        out = torch.empty_like(q)
+    if lse is None and want_lse:
+        lse = torch.empty(B, H, L, dtype=torch.float32, device=q.device)
+    prob = _problem(q, 128, 0, 0, scale)
+    _check(lib.adaspa_dense_attn_lse(ctypes.byref(prob), _ptr(q), _ptr(k), _ptr(v), _ptr(out),
+                                     _ptr(lse), _stream(q.device)))
+    return out, lse
+
+
+@dataclass
+class SearchResult:
+    block_mass: torch.Tensor      # fp32 [B, H, NB, NB]
+    row_ptr: torch.Tensor         # int32 [B*H*NB + 1]
+    col_idx: torch.Tensor         # int32 [capacity]; valid prefix row_ptr[-1]
+    head_k: torch.Tensor          # int32 [B, H]
+    head_recall: torch.Tensor     # fp32 [B, H]
+
+    def nnz(self) -> int:
+        return int(self.row_ptr[-1].item())
+
+
+def _problem_shape(B, H, L, D, block, text_start, text_len, scale):
+    return _Problem(B, H, L, D, block, text_start, text_len, 0.0 if scale is None else float(scale))
+
+
+def block_search_workspace(shape, block, text_start, text_len, mode, head_param_bp,
+                           text_sink=True) -> int:
+    B, H, L, D = shape
+    prob = _problem_shape(B, H, L, D, block, text_start, text_len, None)
+    sel, _keep = _select(mode, head_param_bp, text_sink, False)
+    return int(load_library().adaspa_block_search_workspace(ctypes.byref(prob), ctypes.byref(sel)))
+
+
+def block_search_capacity(shape, block, text_start, text_len, mode, head_param_bp,
+                          text_sink=True) -> int:
+    B, H, L, D = shape
+    prob = _problem_shape(B, H, L, D, block, text_start, text_len, None)
+    sel, _keep = _select(mode, head_param_bp, text_sink, False)
+    return int(load_library().adaspa_block_search_capacity(ctypes.byref(prob), ctypes.byref(sel)))
+
+
+def block_search(q, k, lse, *, block: int, text_start: int, text_len: int,
+                 mode: str, head_param_bp: Sequence[int], text_sink: bool = True,
+                 scale: Optional[float] = None, scores: Optional[torch.Tensor] = None,
+                 shape=None, workspace: Optional[torch.Tensor] = None) -> SearchResult:
+    """Block masses W_sum_attn from ``lse`` (fresh or cached) and the per-head
+    selection.  With ``scores`` given (fp32 [B, H, NB, NB]) the mass pass is
+    skipped and those masses are selected from (then q, k, lse may be None and
+    ``shape`` = (B, H, L, D) is required)."""
+    lib = load_library()
+    given = scores is not None
+    if given:
+        B, H, L, D = shape if shape is not None else q.shape
+        dev = scores.device
+    else:
+        _check_qkv(q, k)
+        B, H, L, D = q.shape
+        dev = q.device
+        if lse.dtype != torch.float32 or not lse.is_contiguous() or lse.shape != (B, H, L):
+            raise AdaspaError("lse must be contiguous fp32 [B, H, L]")
+    nb = (L + block - 1) // block
+    prob = _problem_shape(B, H, L, D, block, text_start, text_len, scale)
+    sel, _keep = _select(mode, head_param_bp, text_sink, given)
+    cap = lib.adaspa_block_search_capacity(ctypes.byref(prob), ctypes.byref(sel))
+    wsb = lib.adaspa_block_search_workspace(ctypes.byref(prob), ctypes.byref(sel))
+    if cap < 0 or wsb == 0:
+        _check(lib.adaspa_block_search(ctypes.byref(prob), None, None, None, ctypes.byref(sel),
+                                       None, None, None, 0, None, None, None, 0, None))
+        raise AdaspaError("invalid block_search arguments")
+    if given:
+        if scores.dtype != torch.float32 or scores.shape != (B, H, nb, nb) or not scores.is_contiguous():
+            raise AdaspaError("scores must be contiguous fp32 [B, H, NB, NB]")
+        mass = scores
+    else:
+        mass = torch.empty(B, H, nb, nb, dtype=torch.float32, device=dev)
+    row_ptr = torch.empty(B * H * nb + 1, dtype=torch.int32, device=dev)
+    col_idx = torch.empty(max(int(cap), 1), dtype=torch.int32, device=dev)
+    head_k = torch.empty(B, H, dtype=torch.int32, device=dev)
+    head_recall = torch.empty(B, H, dtype=torch.float32, device=dev)
+    if workspace is None or workspace.numel() < wsb:
+        workspace = torch.empty(int(wsb), dtype=torch.uint8, device=dev)
+    _check(lib.adaspa_block_search(ctypes.byref(prob), _ptr(q), _ptr(k), _ptr(lse),
+                                   ctypes.byref(sel), _ptr(mass), _ptr(row_ptr), _ptr(col_idx),
+                                   int(col_idx.numel()), _ptr(head_k), _ptr(head_recall),
+                                   _ptr(workspace), int(workspace.numel()), _stream(dev)))
+    return SearchResult(mass, row_ptr, col_idx, head_k, head_recall)
+
+
+def block_sparse_attn(q, k, v, row_ptr, col_idx, *, block: int, scale: Optional[float] = None,
+                      out=None, lse=None, want_lse: bool = True):
+    """Blockified sparse attention over the CSR key-block lists.  Returns (out, lse)."""
+    _check_qkv(q, k, v)
+    lib = load_library()
+    B, H, L, D = q.shape
+    nb = (L + block - 1) // block
+    for t in (row_ptr, col_idx):
+        if t.dtype != torch.int32 or t.device != q.device or not t.is_contiguous():
+            raise AdaspaError("row_ptr and col_idx must be contiguous int32 on q's device")
+    if row_ptr.numel() != B * H * nb + 1:
+        raise AdaspaError(f"row_ptr must have B*H*NB+1 = {B * H * nb + 1} entries")
+    if out is None:
+        out = torch.empty_like(q)
+    if lse is None and want_lse:
+        lse = torch.empty(B, H, L, dtype=torch.float32, device=q.device)
+    prob = _problem(q, block, 0, 0, scale)
+    _check(lib.adaspa_block_sparse_attn(ctypes.byref(prob), _ptr(q), _ptr(k), _ptr(v),
+                                        _ptr(row_ptr), _ptr(col_idx), int(col_idx.numel()),
+                                        _ptr(out), _ptr(lse), _stream(q.device)))
+    return out, lse

@@ -1,0 +1,256 @@
+// C ABI of libadaspa: argument validation on the host, then asynchronous
+// launches on the caller's stream.  No device memory is allocated here.
+#include <math.h>
+#include <string.h>
+
+#pragma GCC visibility push(default)
+#include "adaspa.h"
+#pragma GCC visibility pop
+#include "launch.hpp"
+
+using namespace adaspa;
+
+namespace {
+
+constexpr size_t kAlign = 256;
+
+size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
+
+bool aligned16(const void* p) { return ((uintptr_t)p & 15u) == 0; }
+
+int num_blocks(const adaspa_problem* p) { return (p->seqlen + p->block - 1) / p->block; }
+
+// Common shape checks; returns ADASPA_OK or the status to report.
+adaspa_status check_problem(const adaspa_problem* p) {
+  if (!p) return ADASPA_ERR_INVALID_ARG;
+  if (p->batch < 1 || p->heads < 1 || p->seqlen < 1) return ADASPA_ERR_INVALID_ARG;
+  if (p->text_start < 0 || p->text_len < 0 || p->text_start > p->seqlen ||
+      p->text_len > p->seqlen - p->text_start)
+    return ADASPA_ERR_INVALID_ARG;
+  if (!(isfinite(p->softmax_scale))) return ADASPA_ERR_INVALID_ARG;
+  if (p->head_dim != 64 && p->head_dim != 128) return ADASPA_ERR_UNSUPPORTED;
+  if (p->block != 64 && p->block != 128) return ADASPA_ERR_UNSUPPORTED;
+  // Per-head element offsets are 32-bit inside the kernels.
+  if ((int64_t)p->seqlen * p->head_dim >= ((int64_t)1 << 31)) return ADASPA_ERR_UNSUPPORTED;
+  if ((int64_t)p->batch * p->heads >= 65536) return ADASPA_ERR_UNSUPPORTED;
+  return ADASPA_OK;
+}
+
+float scale_of(const adaspa_problem* p) {
+  return p->softmax_scale > 0.f ? p->softmax_scale : 1.0f / sqrtf((float)p->head_dim);
+}
+
+void text_block_range(const adaspa_problem* p, bool sink, int* lo, int* hi) {
+  if (!sink || p->text_len <= 0) {
+    *lo = 1;
+    *hi = 0;
+    return;
+  }
+  *lo = p->text_start / p->block;
+  *hi = (p->text_start + p->text_len - 1) / p->block;
+}
+
+adaspa_status check_select(const adaspa_problem* p, const adaspa_select* s) {
+  if (!s || !s->head_param_bp) return ADASPA_ERR_INVALID_ARG;
+  if (s->mode != ADASPA_SELECT_TOPK && s->mode != ADASPA_SELECT_COVERAGE) return ADASPA_ERR_UNSUPPORTED;
+  if (s->flags & ~(ADASPA_F_TEXT_SINK | ADASPA_F_SCORES_GIVEN)) return ADASPA_ERR_INVALID_ARG;
+  if (p->heads > kMaxHeads) return ADASPA_ERR_UNSUPPORTED;
+  if (num_blocks(p) > kMaxBlocks) return ADASPA_ERR_UNSUPPORTED;
+  for (int h = 0; h < p->heads; ++h)
+    if (s->head_param_bp[h] < 0 || s->head_param_bp[h] > 10000) return ADASPA_ERR_INVALID_ARG;
+  // Entries of col_idx / row_ptr are int32.
+  int64_t nb = num_blocks(p);
+  if ((int64_t)p->batch * p->heads * nb * nb >= ((int64_t)1 << 31)) return ADASPA_ERR_UNSUPPORTED;
+  return ADASPA_OK;
+}
+
+struct WsLayout {
+  size_t idx, prefix, curve, headk, base, total;
+};
+
+WsLayout workspace_layout(const adaspa_problem* p) {
+  const size_t bh = (size_t)p->batch * p->heads;
+  const size_t nb = (size_t)num_blocks(p);
+  const size_t rows = bh * nb;
+  WsLayout w;
+  size_t off = 0;
+  w.idx = off;    off = align_up(off + rows * nb * sizeof(int32_t));
+  w.prefix = off; off = align_up(off + rows * nb * sizeof(int64_t));
+  w.curve = off;  off = align_up(off + bh * nb * sizeof(int64_t));
+  w.headk = off;  off = align_up(off + bh * sizeof(int32_t));
+  w.base = off;   off = align_up(off + bh * sizeof(int64_t));
+  w.total = off;
+  return w;
+}
+
+int topk_count(int keep_bp, int nb, int n_text) {
+  int64_t k = ((int64_t)keep_bp * nb + 9999) / 10000;
+  int kmin = n_text > 1 ? n_text : 1;
+  if (k > nb) k = nb;
+  if (k < kmin) k = kmin;
+  return (int)k;
+}
+
+}  // namespace
+
+#pragma GCC visibility push(default)
+extern "C" {
+
+const char* adaspa_status_string(adaspa_status s) {
+  switch (s) {
+    case ADASPA_OK: return "ok";
+    case ADASPA_ERR_INVALID_ARG: return "invalid argument";
+    case ADASPA_ERR_UNSUPPORTED: return "unsupported shape or mode";
+    case ADASPA_ERR_CAPACITY: return "col_idx capacity too small";
+    case ADASPA_ERR_WORKSPACE: return "workspace missing or too small";
+    case ADASPA_ERR_HIP: return "HIP launch error";
+  }
+  return "unknown status";
+}
+
+adaspa_status adaspa_dense_attn_lse(const adaspa_problem* prob, const void* q, const void* k,
+                                    const void* v, void* out, float* lse, void* stream) {
+  adaspa_status st = check_problem(prob);
+  if (st != ADASPA_OK) return st;
+  if (!q || !k || !v || !out) return ADASPA_ERR_INVALID_ARG;
+  if (!aligned16(q) || !aligned16(k) || !aligned16(v) || !aligned16(out) ||
+      (lse && ((uintptr_t)lse & 3u)))
+    return ADASPA_ERR_INVALID_ARG;
+  AttnParams a;
+  memset(&a, 0, sizeof a);
+  a.q = (const u16*)q;
+  a.k = (const u16*)k;
+  a.v = (const u16*)v;
+  a.o = (u16*)out;
+  a.lse = lse;
+  a.batch_heads = prob->batch * prob->heads;
+  a.seqlen = prob->seqlen;
+  a.block = prob->block;
+  a.nkb = num_blocks(prob);
+  a.scale = scale_of(prob);
+  a.scale_log2 = a.scale * 1.4426950408889634f;
+  return launch_dense(a, prob->head_dim, (hipStream_t)stream) == hipSuccess ? ADASPA_OK : ADASPA_ERR_HIP;
+}
+
+size_t adaspa_block_search_workspace(const adaspa_problem* prob, const adaspa_select* sel) {
+  if (check_problem(prob) != ADASPA_OK || check_select(prob, sel) != ADASPA_OK) return 0;
+  return workspace_layout(prob).total;
+}
+
+int64_t adaspa_block_search_capacity(const adaspa_problem* prob, const adaspa_select* sel) {
+  if (check_problem(prob) != ADASPA_OK || check_select(prob, sel) != ADASPA_OK) return -1;
+  const int64_t nb = num_blocks(prob);
+  const int64_t bh = (int64_t)prob->batch * prob->heads;
+  if (sel->mode == ADASPA_SELECT_COVERAGE) return bh * nb * nb;
+  int lo, hi;
+  text_block_range(prob, (sel->flags & ADASPA_F_TEXT_SINK) != 0, &lo, &hi);
+  const int n_text = lo <= hi ? hi - lo + 1 : 0;
+  int64_t total = 0;
+  for (int h = 0; h < prob->heads; ++h) {
+    const int k = topk_count(sel->head_param_bp[h], (int)nb, n_text);
+    total += n_text * nb + (nb - n_text) * k;
+  }
+  return total * prob->batch;
+}
+
+adaspa_status adaspa_block_search(const adaspa_problem* prob, const void* q, const void* k,
+                                  const float* lse, const adaspa_select* sel, float* block_mass,
+                                  int32_t* row_ptr, int32_t* col_idx, int64_t col_capacity,
+                                  int32_t* head_k, float* head_recall, void* workspace,
+                                  size_t workspace_bytes, void* stream) {
+  adaspa_status st = check_problem(prob);
+  if (st != ADASPA_OK) return st;
+  st = check_select(prob, sel);
+  if (st != ADASPA_OK) return st;
+  const bool given = (sel->flags & ADASPA_F_SCORES_GIVEN) != 0;
+  if (!block_mass || !row_ptr || !col_idx) return ADASPA_ERR_INVALID_ARG;
+  if (!given) {
+    if (!q || !k || !lse) return ADASPA_ERR_INVALID_ARG;
+    if (!aligned16(q) || !aligned16(k) || ((uintptr_t)lse & 3u)) return ADASPA_ERR_INVALID_ARG;
+  }
+  if (((uintptr_t)block_mass & 3u) || ((uintptr_t)row_ptr & 3u) || ((uintptr_t)col_idx & 3u))
+    return ADASPA_ERR_INVALID_ARG;
+  const int64_t need = adaspa_block_search_capacity(prob, sel);
+  if (col_capacity < need) return ADASPA_ERR_CAPACITY;
+  const WsLayout wl = workspace_layout(prob);
+  if (!workspace || workspace_bytes < wl.total || ((uintptr_t)workspace % kAlign))
+    return ADASPA_ERR_WORKSPACE;
+
+  hipStream_t s = (hipStream_t)stream;
+  const int nb = num_blocks(prob);
+  const int bh = prob->batch * prob->heads;
+  if (!given) {
+    MassParams m;
+    memset(&m, 0, sizeof m);
+    m.q = (const u16*)q;
+    m.k = (const u16*)k;
+    m.lse = lse;
+    m.w = block_mass;
+    m.batch_heads = bh;
+    m.seqlen = prob->seqlen;
+    m.block = prob->block;
+    m.nkb = nb;
+    m.scale_log2 = scale_of(prob) * 1.4426950408889634f;
+    if (launch_block_mass(m, prob->head_dim, s) != hipSuccess) return ADASPA_ERR_HIP;
+  }
+
+  SelectParams P;
+  memset(&P, 0, sizeof P);
+  char* ws = (char*)workspace;
+  P.w = block_mass;
+  P.row_ptr = row_ptr;
+  P.col_idx = col_idx;
+  P.head_k_out = head_k;
+  P.head_recall_out = head_recall;
+  P.ws_idx = (int32_t*)(ws + wl.idx);
+  P.ws_prefix = (int64_t*)(ws + wl.prefix);
+  P.ws_curve = (int64_t*)(ws + wl.curve);
+  P.ws_headk = (int32_t*)(ws + wl.headk);
+  P.ws_base = (int64_t*)(ws + wl.base);
+  P.batch_heads = bh;
+  P.heads = prob->heads;
+  P.nb = nb;
+  text_block_range(prob, (sel->flags & ADASPA_F_TEXT_SINK) != 0, &P.text_lo, &P.text_hi);
+  const int n_text = P.text_lo <= P.text_hi ? P.text_hi - P.text_lo + 1 : 0;
+  P.kmin = n_text > 1 ? n_text : 1;
+  P.mode = sel->mode;
+  P.cap = (int64_t)((((uint64_t)1) << 62) / ((uint64_t)nb * (uint64_t)nb));
+  for (int h = 0; h < prob->heads; ++h)
+    P.head_param[h] = sel->mode == ADASPA_SELECT_TOPK ? topk_count(sel->head_param_bp[h], nb, n_text)
+                                                      : sel->head_param_bp[h];
+  return launch_select(P, s) == hipSuccess ? ADASPA_OK : ADASPA_ERR_HIP;
+}
+
+adaspa_status adaspa_block_sparse_attn(const adaspa_problem* prob, const void* q, const void* k,
+                                       const void* v, const int32_t* row_ptr,
+                                       const int32_t* col_idx, int64_t col_count, void* out,
+                                       float* lse_out, void* stream) {
+  adaspa_status st = check_problem(prob);
+  if (st != ADASPA_OK) return st;
+  if (!q || !k || !v || !out || !row_ptr || (!col_idx && col_count > 0) || col_count < 0)
+    return ADASPA_ERR_INVALID_ARG;
+  if (!aligned16(q) || !aligned16(k) || !aligned16(v) || !aligned16(out) ||
+      (lse_out && ((uintptr_t)lse_out & 3u)) || ((uintptr_t)row_ptr & 3u) ||
+      ((uintptr_t)col_idx & 3u))
+    return ADASPA_ERR_INVALID_ARG;
+  AttnParams a;
+  memset(&a, 0, sizeof a);
+  a.q = (const u16*)q;
+  a.k = (const u16*)k;
+  a.v = (const u16*)v;
+  a.o = (u16*)out;
+  a.lse = lse_out;
+  a.row_ptr = row_ptr;
+  a.col_idx = col_idx;
+  a.col_count = col_count;
+  a.batch_heads = prob->batch * prob->heads;
+  a.seqlen = prob->seqlen;
+  a.block = prob->block;
+  a.nkb = num_blocks(prob);
+  a.scale = scale_of(prob);
+  a.scale_log2 = a.scale * 1.4426950408889634f;
+  return launch_sparse(a, prob->head_dim, (hipStream_t)stream) == hipSuccess ? ADASPA_OK : ADASPA_ERR_HIP;
+}
+
+}  // extern "C"
+#pragma GCC visibility pop

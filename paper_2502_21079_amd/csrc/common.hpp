@@ -1,0 +1,53 @@
+// Shared device helpers for the gfx950 (CDNA4) kernels of the AdaSpa path.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace adaspa {
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+typedef short s16x4 __attribute__((ext_vector_type(4)));
+typedef uint16_t u16;
+
+constexpr float kLog2e = 1.4426950408889634f;
+constexpr float kLn2 = 0.6931471805599453f;
+
+// C[32x32] += A[32x16] * B[16x32] on bf16 inputs, fp32 accumulate.
+// Lane l supplies A[l%32][8*(l/32) + e] and B[8*(l/32) + e][l%32], e = 0..7;
+// accumulator element 4*i + j of lane l is C[8*i + 4*(l/32) + j][l%32].
+__device__ __forceinline__ f32x16 mfma32(bf16x8 a, bf16x8 b, f32x16 c) {
+  return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
+}
+
+// LDS transpose read of 16-bit elements.  Within each group of 16 lanes, lane
+// j names 4 consecutive elements R[j][0..3]; lane i receives R[i/4 + 4e][i%4]
+// for e = 0..3.
+__device__ __forceinline__ s16x4 lds_read_tr16(const u16* p) {
+  return __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+      (__attribute__((address_space(3))) s16x4*)(p));
+}
+
+__device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
+
+// Workgroups are dispatched round-robin over the 8 XCDs (workgroup i runs on
+// XCD i % 8).  Map hardware id -> logical id so that each XCD receives one
+// contiguous range of logical ids: neighbouring tiles of one head then share
+// that XCD's L2.  Bijective for any n.
+__device__ __forceinline__ int xcd_remap(int bid, int n) {
+  const int nx = 8;
+  int q = n / nx, r = n % nx;
+  int x = bid % nx, k = bid / nx;
+  int off = x * q + (x < r ? x : r);
+  return off + k;
+}
+
+__device__ __forceinline__ float wave_sum(float v) {
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) v += __shfl_xor(v, o, 64);
+  return v;
+}
+
+}  // namespace adaspa

@@ -1,0 +1,146 @@
+"""CPU checks of the C-ABI library: it loads, exports every symbol the header
+declares, and rejects invalid arguments synchronously (before any GPU work).
+
+Only validation paths and pure host helpers are called here: no kernel runs.
+"""
+import ctypes
+import os
+import re
+
+import pytest
+
+import paper_2502_21079_amd as ad
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "adaspa.h")
+
+
+def _declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(adaspa_[a-z_]+)\s*\(", text)))
+
+
+@pytest.fixture(scope="module")
+def lib():
+    return ad.load_library()
+
+
+def test_header_declares_the_binding_symbols():
+    assert _declared_functions() == sorted(ad.EXPORTED_SYMBOLS)
+
+
+def test_library_exports_every_declared_symbol(lib):
+    for name in _declared_functions():
+        assert hasattr(lib, name), name
+        assert getattr(lib, name) is not None
+
+
+def test_status_strings(lib):
+    for code in range(6):
+        assert lib.adaspa_status_string(code)
+    assert lib.adaspa_status_string(0) == b"ok"
+
+
+def _prob(**kw):
+    base = dict(batch=1, heads=2, seqlen=2048, head_dim=64, block=64, text_start=0,
+                text_len=64, softmax_scale=0.0)
+    base.update(kw)
+    return ad._Problem(*[base[f] for f, _ in ad._Problem._fields_])
+
+
+def _sel(mode=0, flags=1, params=(2000, 2000)):
+    arr = (ctypes.c_int32 * len(params))(*params)
+    return ad._Select(mode, flags, ctypes.cast(arr, ctypes.POINTER(ctypes.c_int32))), arr
+
+
+FAKE = ctypes.c_void_p(0x10000)     # aligned, never dereferenced: validation fails first
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(head_dim=96), 2), (dict(head_dim=256), 2), (dict(block=32), 2), (dict(block=256), 2),
+    (dict(seqlen=0), 1), (dict(batch=0), 1), (dict(heads=0), 1),
+    (dict(text_start=2000, text_len=100), 1), (dict(text_len=-1), 1),
+    (dict(softmax_scale=float("nan")), 1), (dict(softmax_scale=float("inf")), 1),
+])
+def test_dense_rejects_bad_problems(lib, kw, status):
+    p = _prob(**kw)
+    assert lib.adaspa_dense_attn_lse(ctypes.byref(p), FAKE, FAKE, FAKE, FAKE, None, None) == status
+
+
+def test_dense_rejects_null_and_misaligned(lib):
+    p = _prob()
+    assert lib.adaspa_dense_attn_lse(None, FAKE, FAKE, FAKE, FAKE, None, None) == 1
+    assert lib.adaspa_dense_attn_lse(ctypes.byref(p), None, FAKE, FAKE, FAKE, None, None) == 1
+    assert lib.adaspa_dense_attn_lse(ctypes.byref(p), ctypes.c_void_p(0x10008), FAKE, FAKE, FAKE,
+                                     None, None) == 1
+    assert lib.adaspa_dense_attn_lse(ctypes.byref(p), FAKE, FAKE, FAKE, FAKE,
+                                     ctypes.c_void_p(0x10002), None) == 1
+
+
+def test_capacity_and_workspace(lib):
+    p = _prob()
+    s, _a = _sel(mode=0, params=(2000, 5000))
+    nb = 32
+    # one text block -> text row keeps 32; video rows keep ceil(0.2*32)=7 / 16
+    expect = (nb + (nb - 1) * 7) + (nb + (nb - 1) * 16)
+    assert lib.adaspa_block_search_capacity(ctypes.byref(p), ctypes.byref(s)) == expect
+    s2, _b = _sel(mode=1, params=(9000, 9000))
+    assert lib.adaspa_block_search_capacity(ctypes.byref(p), ctypes.byref(s2)) == 2 * nb * nb
+    ws = lib.adaspa_block_search_workspace(ctypes.byref(p), ctypes.byref(s2))
+    assert ws >= 2 * nb * nb * 12 and ws % 256 == 0
+    bad, _c = _sel(mode=1, params=(9000, 10001))
+    assert lib.adaspa_block_search_workspace(ctypes.byref(p), ctypes.byref(bad)) == 0
+    assert lib.adaspa_block_search_capacity(ctypes.byref(p), ctypes.byref(bad)) == -1
+    bad2, _d = _sel(mode=7)
+    assert lib.adaspa_block_search_capacity(ctypes.byref(p), ctypes.byref(bad2)) == -1
+
+
+def test_capacity_matches_oracle_counts(lib):
+    import oracle
+    for keep in (0, 1, 500, 1000, 2000, 5000, 10000):
+        p = _prob(seqlen=110336, heads=1, head_dim=128, block=128, text_len=256)
+        s, _a = _sel(mode=0, params=(keep,))
+        k = oracle.topk_count(keep, 862, 2)
+        assert lib.adaspa_block_search_capacity(ctypes.byref(p), ctypes.byref(s)) == 2 * 862 + 860 * k
+
+
+def test_search_rejects_bad_arguments(lib):
+    p = _prob()
+    s, _a = _sel()
+    ws = lib.adaspa_block_search_workspace(ctypes.byref(p), ctypes.byref(s))
+    cap = lib.adaspa_block_search_capacity(ctypes.byref(p), ctypes.byref(s))
+    args = lambda **o: [o.get("prob", ctypes.byref(p)), FAKE, FAKE, FAKE, o.get("sel", ctypes.byref(s)),
+                        FAKE, FAKE, FAKE, o.get("cap", cap), None, None, o.get("ws", FAKE),
+                        o.get("wsb", ws), None]
+    assert lib.adaspa_block_search(*args(cap=cap - 1)) == 3
+    assert lib.adaspa_block_search(*args(wsb=ws - 1)) == 4
+    assert lib.adaspa_block_search(*args(ws=None)) == 4
+    assert lib.adaspa_block_search(*args(ws=ctypes.c_void_p(0x10010))) == 4
+    assert lib.adaspa_block_search(*args(sel=None)) == 1
+    s_bad, _b = _sel(flags=8)
+    assert lib.adaspa_block_search(*args(sel=ctypes.byref(s_bad))) == 1
+    big = _prob(heads=600)
+    arr = (ctypes.c_int32 * 600)(*([1000] * 600))
+    s_big = ad._Select(0, 1, ctypes.cast(arr, ctypes.POINTER(ctypes.c_int32)))
+    assert lib.adaspa_block_search(ctypes.byref(big), FAKE, FAKE, FAKE, ctypes.byref(s_big), FAKE,
+                                   FAKE, FAKE, 10 ** 9, None, None, FAKE, 10 ** 12, None) == 2
+
+
+def test_sparse_rejects_bad_arguments(lib):
+    p = _prob()
+    assert lib.adaspa_block_sparse_attn(ctypes.byref(p), FAKE, FAKE, FAKE, None, FAKE, 10, FAKE,
+                                        None, None) == 1
+    assert lib.adaspa_block_sparse_attn(ctypes.byref(p), FAKE, FAKE, FAKE, FAKE, FAKE, -1, FAKE,
+                                        None, None) == 1
+    assert lib.adaspa_block_sparse_attn(ctypes.byref(p), FAKE, FAKE, FAKE, FAKE,
+                                        ctypes.c_void_p(0x10001), 10, FAKE, None, None) == 1
+    assert lib.adaspa_block_sparse_attn(ctypes.byref(_prob(head_dim=80)), FAKE, FAKE, FAKE, FAKE,
+                                        FAKE, 10, FAKE, None, None) == 2
+
+
+def test_binding_raises_without_library(monkeypatch, tmp_path):
+    monkeypatch.setattr(ad, "_lib", None)
+    monkeypatch.setenv("ADASPA_LIB", str(tmp_path / "missing.so"))
+    with pytest.raises(ad.AdaspaError):
+        ad.load_library()

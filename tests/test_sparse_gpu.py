@@ -1,0 +1,110 @@
+"""GPU parity of adaspa_block_sparse_attn (Sec. 4.1 blockified sparse
+attention) against the fp64 oracle, on seeded block patterns."""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import paper_2502_21079_amd as ad
+from workloads import LONG, TINY, make_qkv, random_block_lists, text_blocks
+from _helpers import check_lse, check_out, f64, sample_blocks
+
+pytestmark = pytest.mark.gpu
+
+
+def _all_blocks(B, H, nb):
+    row_ptr = torch.arange(B * H * nb + 1, dtype=torch.int32) * nb
+    col_idx = torch.arange(nb, dtype=torch.int32).repeat(B * H * nb)
+    return row_ptr.cuda(), col_idx.cuda()
+
+
+@pytest.mark.parametrize("D,block,L", [(64, 64, 2048), (128, 128, 1000), (128, 64, 777), (64, 128, 4096)])
+def test_all_blocks_equals_dense_bitwise(D, block, L):
+    """P1 on the GPU: keeping every block reproduces the dense kernel bit for bit."""
+    w = TINY.replace(head_dim=D, block=block, seqlen=L, patches=(L - 64 + 3) // 4)
+    q, k, v = make_qkv(w, device="cuda")
+    od, ld = ad.dense_attn_lse(q, k, v)
+    rp, ci = _all_blocks(1, w.heads, w.nblocks)
+    os_, ls = ad.block_sparse_attn(q, k, v, rp, ci, block=block)
+    torch.cuda.synchronize()
+    assert torch.equal(od, os_) and torch.equal(ld, ls)
+
+
+def _pattern(nrows, nb, k, seed, always):
+    return random_block_lists(nrows, nb, k, seed, always=always)
+
+
+@pytest.mark.parametrize("D,block,L,k", [(64, 64, 2048, 6), (128, 128, 1000, 3), (128, 64, 777, 4),
+                                         (64, 128, 2048, 1)])
+def test_sparse_matches_oracle(D, block, L, k):
+    w = TINY.replace(head_dim=D, block=block, seqlen=L, patches=(L - 64 + 3) // 4)
+    q, k_, v = make_qkv(w, device="cuda")
+    nb = w.nblocks
+    tb = text_blocks(L, block, 0, 64)
+    rp, ci = _pattern(w.heads * nb, nb, k, seed=L + k, always=tb)
+    out, lse = ad.block_sparse_attn(q, k_, v, rp.cuda(), ci.cuda(), block=block)
+    torch.cuda.synchronize()
+    rpn, cin = rp.numpy(), ci.numpy()
+    for h in range(w.heads):
+        o_ref, l_ref = oracle.block_sparse_attention(f64(q[0, h]), f64(k_[0, h]), f64(v[0, h]),
+                                                     rpn[h * nb:(h + 1) * nb + 1], cin, w.scale, block)
+        check_out(out[0, h], o_ref, f"h{h}")
+        check_lse(lse[0, h], l_ref)
+
+
+def test_sparse_long_sampled():
+    """The 110K-token shape at about 20% density, sampled query blocks."""
+    w = LONG
+    q, k, v = make_qkv(w, device="cuda")
+    nb = w.nblocks
+    kk = oracle.topk_count(2000, nb, 2)
+    rp, ci = _pattern(w.heads * nb, nb, kk, seed=5, always=[0, 1])
+    out, lse = ad.block_sparse_attn(q, k, v, rp.cuda(), ci.cuda(), block=w.block)
+    torch.cuda.synchronize()
+    rpn, cin = rp.numpy(), ci.numpy()
+    for h in (0, 13, 23):
+        blocks = sample_blocks(nb, 3, seed=400 + h, always=(0, 2))
+        o_ref, l_ref = oracle.block_sparse_attention(f64(q[0, h]), f64(k[0, h]), f64(v[0, h]),
+                                                     rpn[h * nb:(h + 1) * nb + 1], cin, w.scale,
+                                                     w.block, qblocks=blocks)
+        rows = np.concatenate([np.arange(p * 128, min((p + 1) * 128, w.seqlen)) for p in blocks])
+        idx = torch.as_tensor(rows, device="cuda")
+        check_out(out[0, h, idx], o_ref, f"h{h}")
+        check_lse(lse[0, h, idx], l_ref)
+
+
+def test_empty_rows_and_skipped_indices():
+    """A row with no kept block gives zeros and LSE -inf; entries outside
+    [0, NB) are skipped by the kernel's own bounds check."""
+    w = TINY.replace(seqlen=512, patches=112)
+    q, k, v = make_qkv(w, device="cuda")
+    nb = 8
+    rows = []
+    for r in range(w.heads * nb):
+        rows.append([] if r % 3 == 0 else [r % nb])
+    rows[1] = [-1, 2, 99]           # out-of-range entries around a valid one
+    row_ptr = torch.tensor([0] + list(np.cumsum([len(x) for x in rows])), dtype=torch.int32)
+    col_idx = torch.tensor([c for x in rows for c in x], dtype=torch.int32)
+    out, lse = ad.block_sparse_attn(q, k, v, row_ptr.cuda(), col_idx.cuda(), block=64)
+    torch.cuda.synchronize()
+    for r, kept in enumerate(rows):
+        h, p = divmod(r, nb)
+        valid = [c for c in kept if 0 <= c < nb]
+        mask = oracle.key_mask_from_blocks(valid, 512, 64)
+        o_ref, l_ref = oracle.masked_attention(f64(q[0, h, p * 64:(p + 1) * 64]), f64(k[0, h]),
+                                               f64(v[0, h]), mask, w.scale)
+        check_out(out[0, h, p * 64:(p + 1) * 64], o_ref, f"row {r}")
+        check_lse(lse[0, h, p * 64:(p + 1) * 64], l_ref)
+        if not valid:
+            assert torch.all(out[0, h, p * 64:(p + 1) * 64] == 0)
+
+
+def test_sparse_deterministic():
+    w = TINY.replace(head_dim=128, block=128)
+    q, k, v = make_qkv(w, device="cuda")
+    rp, ci = _pattern(w.heads * w.nblocks, w.nblocks, 5, seed=1, always=[0])
+    rp, ci = rp.cuda(), ci.cuda()
+    o1, l1 = ad.block_sparse_attn(q, k, v, rp, ci, block=128)
+    o2, l2 = ad.block_sparse_attn(q, k, v, rp, ci, block=128)
+    torch.cuda.synchronize()
+    assert torch.equal(o1, o2) and torch.equal(l1, l2)
