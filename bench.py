@@ -1,0 +1,274 @@
+"""Benchmark of the AdaSpa attention hot path on one MI355X.
+
+One step is one pass of the whole path over the long-video workload
+(B=1, H=24, d=128, L=110,336 = 256 text + 32 frames x 3,440 patches,
+block 128, bf16 Q/K/V from the structured generator):
+
+    dense attention + LSE  ->  block search (masses from the fresh LSE,
+    per-head coverage target 0.9 with text sink)  ->  block-sparse attention
+
+Inputs are resident in HBM before the timed region.  Each kernel call is
+bracketed by HIP events on the stream it runs on; the JSON line reports the
+block-sparse effective TFLOP/s over the kept blocks as ``value``, every
+kernel's time and roofline fraction, the density sweep (keep 5/10/20/50% and
+a per-head mix) with the speedup over dense, and the fp64 CPU oracle timed on
+a bounded sample on this host.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import math
+import os
+import sys
+import time
+
+import numpy as np
+import torch
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+import paper_2502_21079_amd as ad  # noqa: E402
+from workloads import LONG, make_qkv  # noqa: E402
+
+PEAK_BF16_TFLOPS = 2500.0     # MI355X dense bf16 MFMA
+PEAK_HBM_GBS = 8000.0
+
+
+def attn_flops(L: int, D: int, H: int, B: int = 1) -> float:
+    """QK^T and PV, 2 flops per multiply-add: 4 L^2 D per head."""
+    return 4.0 * L * L * D * H * B
+
+
+def sparse_flops(nnz_blocks: int, block: int, D: int) -> float:
+    return 4.0 * D * block * block * nnz_blocks
+
+
+def mass_flops(L: int, D: int, H: int, B: int = 1) -> float:
+    return 2.0 * L * L * D * H * B
+
+
+class Timer:
+    """Accumulates HIP-event time of enqueued work on the current stream."""
+
+    def __init__(self):
+        self.pending = {}
+        self.done = {}
+
+    def __call__(self, name, fn, *a, **kw):
+        s, e = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        s.record()
+        r = fn(*a, **kw)
+        e.record()
+        self.pending.setdefault(name, []).append((s, e))
+        return r
+
+    def collect(self):
+        torch.cuda.synchronize()
+        for k, evs in self.pending.items():
+            self.done.setdefault(k, []).extend(s.elapsed_time(e) for s, e in evs)
+        self.pending = {}
+        return self.done
+
+
+def cpu_oracle_baseline(q, k, v, w, budget_s: float):
+    """The fp64 oracle's dense attention + LSE on sampled query blocks, one
+    per head in turn, until ``budget_s`` seconds of CPU work have run."""
+    import oracle
+    try:
+        from threadpoolctl import threadpool_info
+        threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
+    except Exception:  # pragma: no cover
+        threads = os.cpu_count() or 1
+    rng = np.random.default_rng(0)
+    nb = w.nblocks
+    flops = 0.0
+    blocks = 0
+    t0 = time.perf_counter()
+    elapsed = 0.0
+    kv_cache = {}
+    while True:
+        h = blocks % w.heads
+        p = int(rng.integers(0, nb))
+        if h not in kv_cache:
+            kv_cache = {h: (k[0, h].float().cpu().numpy().astype(np.float64),
+                            v[0, h].float().cpu().numpy().astype(np.float64))}
+        kh, vh = kv_cache[h]
+        qb = q[0, h, p * w.block:(p + 1) * w.block].float().cpu().numpy().astype(np.float64)
+        ts = time.perf_counter()
+        oracle.dense_attention(qb, kh, vh, w.scale)
+        t_used = time.perf_counter() - ts
+        flops += 4.0 * qb.shape[0] * w.seqlen * w.head_dim
+        blocks += 1
+        elapsed += t_used
+        if elapsed >= budget_s or blocks >= 4 * w.heads:
+            break
+    return {"value": round(flops / elapsed / 1e12, 6), "unit": "TFLOP/s",
+            "cores": int(threads), "kind": "oracle",
+            "host_cpus": os.cpu_count(),
+            "sample": (f"fp64 oracle dense attention + LSE (numpy/BLAS) on {blocks} query blocks "
+                       f"of 128 rows x {w.seqlen} keys, d={w.head_dim}, heads taken in turn; "
+                       f"{elapsed:.1f} s of compute; effective TFLOP/s = 4*rows*L*d / time"),
+            "total_wall_s": round(time.perf_counter() - t0, 1)}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=5)
+    ap.add_argument("--warmup", type=int, default=2)
+    ap.add_argument("--coverage-bp", type=int, default=LONG.coverage_bp)
+    ap.add_argument("--no-sweep", action="store_true")
+    ap.add_argument("--cpu-budget", type=float, default=12.0)
+    ap.add_argument("--no-cpu", action="store_true")
+    ap.add_argument("--kernel", choices=["all", "dense", "sparse", "search", "copy"], default="all",
+                    help="profile helper: run only one kernel in the timed loop; 'copy' runs a "
+                         "plain 1 GiB device copy, the reference for HBM byte counters")
+    args = ap.parse_args()
+
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        print("bench.py measures one GPU only: the AdaSpa path here is single-GPU "
+              "(heads would shard across GPUs with no exchange); run with --gpus 1.",
+              file=sys.stderr, flush=True)
+        sys.exit(2)
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    ad.load_library()
+    if args.kernel == "copy":
+        src = torch.empty(1 << 29, dtype=torch.int16, device="cuda").fill_(1)   # 1 GiB
+        dst = torch.empty_like(src)
+        for _ in range(max(1, args.steps)):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        print(f"[bench] copied {src.numel() * 2} bytes x {max(1, args.steps)}", file=sys.stderr, flush=True)
+        return
+
+    w = LONG
+    B, H, L, D, blk = w.batch, w.heads, w.seqlen, w.head_dim, w.block
+    nb = w.nblocks
+    print(f"[bench] generating {w.name}", file=sys.stderr, flush=True)
+    q, k, v = make_qkv(w, device="cuda")
+    out = torch.empty_like(q)
+    lse = torch.empty(B, H, L, dtype=torch.float32, device="cuda")
+    sp_out = torch.empty_like(q)
+    tau = [args.coverage_bp] * H
+    wsb = ad.block_search_workspace((B, H, L, D), blk, w.text_start, w.text_len, "coverage", tau)
+    ws = torch.empty(wsb, dtype=torch.uint8, device="cuda")
+    torch.cuda.synchronize()
+
+    def step(t: Timer):
+        if args.kernel in ("all", "dense"):
+            t("dense", ad.dense_attn_lse, q, k, v, out=out, lse=lse)
+        res = None
+        if args.kernel in ("all", "search"):
+            res = t("search", ad.block_search, q, k, lse, block=blk, text_start=w.text_start,
+                    text_len=w.text_len, mode="coverage", head_param_bp=tau, workspace=ws)
+        if args.kernel in ("all", "sparse"):
+            rp, ci = step.pattern if res is None else (res.row_ptr, res.col_idx)
+            t("sparse", ad.block_sparse_attn, q, k, v, rp, ci, block=blk, out=sp_out, want_lse=False)
+        return res
+
+    # pattern for a sparse-only profile run
+    if args.kernel == "sparse":
+        ad.dense_attn_lse(q, k, v, out=out, lse=lse)
+        r0 = ad.block_search(q, k, lse, block=blk, text_start=w.text_start, text_len=w.text_len,
+                             mode="coverage", head_param_bp=tau, workspace=ws)
+        step.pattern = (r0.row_ptr, r0.col_idx)
+
+    print(f"[bench] warmup {args.warmup}", file=sys.stderr, flush=True)
+    for _ in range(args.warmup):
+        step(Timer())
+    torch.cuda.synchronize()
+    timer = Timer()
+    print(f"[bench] timing {args.steps} steps", file=sys.stderr, flush=True)
+    t0 = time.perf_counter()
+    res = None
+    for _ in range(args.steps):
+        res = step(timer)
+    torch.cuda.synchronize()
+    wall_ms = (time.perf_counter() - t0) * 1e3 / args.steps
+    ev = {kname: float(np.mean(v_)) for kname, v_ in timer.collect().items()}
+    print(f"[bench] step ms {wall_ms:.2f} kernels {ev}", file=sys.stderr, flush=True)
+    if args.kernel != "all":
+        return
+
+    nnz = res.nnz()
+    head_k = res.head_k.cpu().numpy()[0]
+    head_rec = res.head_recall.cpu().numpy()[0]
+    f_dense = attn_flops(L, D, H, B)
+    f_sparse = sparse_flops(nnz, blk, D)
+    f_mass = mass_flops(L, D, H, B)
+    dense_ms, search_ms, sparse_ms = ev["dense"], ev["search"], ev["sparse"]
+    tf = lambda f, ms: f / (ms * 1e-3) / 1e12
+    kernels = {
+        "dense_attn_lse": {"ms": round(dense_ms, 3), "tflops": round(tf(f_dense, dense_ms), 1),
+                           "frac_bf16_peak": round(tf(f_dense, dense_ms) / PEAK_BF16_TFLOPS, 4)},
+        "block_search": {"ms": round(search_ms, 3),
+                         "mass_tflops_equiv": round(tf(f_mass, search_ms), 1),
+                         "vs_dense": round(search_ms / dense_ms, 4)},
+        "block_sparse_attn": {"ms": round(sparse_ms, 3), "tflops": round(tf(f_sparse, sparse_ms), 1),
+                              "frac_bf16_peak": round(tf(f_sparse, sparse_ms) / PEAK_BF16_TFLOPS, 4),
+                              "nnz_blocks": nnz, "density": round(nnz / (B * H * nb * nb), 5),
+                              "speedup_vs_dense": round(dense_ms / sparse_ms, 3)},
+    }
+    detail = {"head_k": head_k.tolist(), "head_recall_min": float(head_rec.min()),
+              "head_recall_mean": float(head_rec.mean())}
+
+    # density sweep: selection from the same masses at fixed keep fractions
+    sweep = {}
+    if not args.no_sweep:
+        print("[bench] density sweep", file=sys.stderr, flush=True)
+        mix_rng = np.random.default_rng(3)
+        mix = [int(x) for x in mix_rng.integers(500, 5001, size=H)]
+        for name, params in [("keep5", [500] * H), ("keep10", [1000] * H), ("keep20", [2000] * H),
+                             ("keep50", [5000] * H), ("mix5to50", mix)]:
+            r = ad.block_search(None, None, None, block=blk, text_start=w.text_start,
+                                text_len=w.text_len, mode="topk", head_param_bp=params,
+                                scores=res.block_mass, shape=(B, H, L, D))
+            tm = Timer()
+            for _ in range(2):
+                ad.block_sparse_attn(q, k, v, r.row_ptr, r.col_idx, block=blk, out=sp_out, want_lse=False)
+            for _ in range(max(3, args.steps)):
+                tm("s", ad.block_sparse_attn, q, k, v, r.row_ptr, r.col_idx, block=blk, out=sp_out,
+                   want_lse=False)
+            ms = float(np.mean(tm.collect()["s"]))
+            nz = r.nnz()
+            hk = r.head_k.cpu().numpy()[0].astype(np.float64)
+            sweep[name] = {"ms": round(ms, 3), "tflops": round(tf(sparse_flops(nz, blk, D), ms), 1),
+                           "frac_bf16_peak": round(tf(sparse_flops(nz, blk, D), ms) / PEAK_BF16_TFLOPS, 4),
+                           "density": round(nz / (B * H * nb * nb), 4),
+                           "speedup_vs_dense": round(dense_ms / ms, 3),
+                           "head_imbalance": round(float(hk.max() / hk.mean()), 3)}
+
+    cpu = None
+    if not args.no_cpu:
+        print("[bench] cpu oracle baseline", file=sys.stderr, flush=True)
+        cpu = cpu_oracle_baseline(q, k, v, w, args.cpu_budget)
+
+    roof = {"kernel": "dense_attn_lse", "bound": "mfma", "achieved": round(tf(f_dense, dense_ms), 1),
+            "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
+            "frac": round(tf(f_dense, dense_ms) / PEAK_BF16_TFLOPS, 4), "traffic": None,
+            "algorithmic_flops_per_launch": f_dense}
+    line = {
+        "metric": "block-sparse attn ms + effective TFLOP/s @110K tok,24h,d128; search ms vs dense",
+        "value": round(tf(f_sparse, sparse_ms), 2),
+        "unit": "TFLOP/s",
+        "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
+        "ms_per_step": round(wall_ms, 3),
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+        "dtype": "bf16", "data": "synthetic",
+        "config": {"workload": w.name, "batch": B, "heads": H, "seq_len": L, "head_dim": D,
+                   "block": blk, "text_tokens": w.text_len, "frames": w.frames,
+                   "patches_per_frame": w.patches, "selection": f"coverage tau={args.coverage_bp}bp",
+                   "step": "dense_attn_lse -> block_search -> block_sparse_attn"},
+        "sparse_ms": round(sparse_ms, 3), "dense_ms": round(dense_ms, 3), "search_ms": round(search_ms, 3),
+        "search_vs_dense": round(search_ms / dense_ms, 4),
+        "kernels": kernels, "density_sweep": sweep, "detail": detail,
+        "roofline": roof, "cpu_baseline": cpu,
+    }
+    print(json.dumps(line), flush=True)
+
+
+if __name__ == "__main__":
+    main()
