@@ -121,6 +121,9 @@ def main():
     ap.add_argument("--coverage-bp", type=int, default=LONG.coverage_bp)
     ap.add_argument("--no-sweep", action="store_true")
     ap.add_argument("--cpu-budget", type=float, default=12.0)
+    ap.add_argument("--sparse-keep", type=int, default=0,
+                    help="with --kernel sparse: per-head keep fraction (basis points, TOPK) "
+                         "instead of the coverage selection")
     ap.add_argument("--no-cpu", action="store_true")
     ap.add_argument("--kernel", choices=["all", "dense", "sparse", "search", "copy"], default="all",
                     help="profile helper: run only one kernel in the timed loop; 'copy' runs a "
@@ -172,8 +175,12 @@ def main():
     # pattern for a sparse-only profile run
     if args.kernel == "sparse":
         ad.dense_attn_lse(q, k, v, out=out, lse=lse)
-        r0 = ad.block_search(q, k, lse, block=blk, text_start=w.text_start, text_len=w.text_len,
-                             mode="coverage", head_param_bp=tau, workspace=ws)
+        if args.sparse_keep > 0:
+            r0 = ad.block_search(q, k, lse, block=blk, text_start=w.text_start, text_len=w.text_len,
+                                 mode="topk", head_param_bp=[args.sparse_keep] * H)
+        else:
+            r0 = ad.block_search(q, k, lse, block=blk, text_start=w.text_start, text_len=w.text_len,
+                                 mode="coverage", head_param_bp=tau, workspace=ws)
         step.pattern = (r0.row_ptr, r0.col_idx)
 
     print(f"[bench] warmup {args.warmup}", file=sys.stderr, flush=True)

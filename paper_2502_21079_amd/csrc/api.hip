@@ -1,6 +1,7 @@
 // C ABI of libadaspa: argument validation on the host, then asynchronous
 // launches on the caller's stream.  No device memory is allocated here.
 #include <math.h>
+#include <stdlib.h>
 #include <string.h>
 
 #pragma GCC visibility push(default)
@@ -93,6 +94,22 @@ int topk_count(int keep_bp, int nb, int n_text) {
 
 }  // namespace
 
+namespace adaspa {
+// Work-to-XCD mapping (see the kernels): 1 gives each XCD one contiguous range
+// of (head, query tile) work items, so the workgroups sharing an L2 stream the
+// same K/V (dense attention and the mass pass: about 6x less HBM traffic than
+// hardware order); 0 keeps the hardware's round-robin order, which balances
+// heads of different cost (block-sparse attention with per-head densities);
+// 2 is the head-chunked order.  ADASPA_XCD_MAP overrides the per-kernel choice.
+int xcd_map_mode(int kernel_default) {
+  static const int env = [] {
+    const char* e = getenv("ADASPA_XCD_MAP");
+    return e ? atoi(e) : -1;
+  }();
+  return env >= 0 ? env : kernel_default;
+}
+}  // namespace adaspa
+
 #pragma GCC visibility push(default)
 extern "C" {
 
@@ -129,6 +146,7 @@ adaspa_status adaspa_dense_attn_lse(const adaspa_problem* prob, const void* q, c
   a.nkb = num_blocks(prob);
   a.scale = scale_of(prob);
   a.scale_log2 = a.scale * 1.4426950408889634f;
+  a.xcd_map = xcd_map_mode(1);
   return launch_dense(a, prob->head_dim, (hipStream_t)stream) == hipSuccess ? ADASPA_OK : ADASPA_ERR_HIP;
 }
 
@@ -191,6 +209,7 @@ adaspa_status adaspa_block_search(const adaspa_problem* prob, const void* q, con
     m.block = prob->block;
     m.nkb = nb;
     m.scale_log2 = scale_of(prob) * 1.4426950408889634f;
+    m.xcd_map = xcd_map_mode(1);
     if (launch_block_mass(m, prob->head_dim, s) != hipSuccess) return ADASPA_ERR_HIP;
   }
 
@@ -249,6 +268,7 @@ adaspa_status adaspa_block_sparse_attn(const adaspa_problem* prob, const void* q
   a.nkb = num_blocks(prob);
   a.scale = scale_of(prob);
   a.scale_log2 = a.scale * 1.4426950408889634f;
+  a.xcd_map = xcd_map_mode(0);
   return launch_sparse(a, prob->head_dim, (hipStream_t)stream) == hipSuccess ? ADASPA_OK : ADASPA_ERR_HIP;
 }
 

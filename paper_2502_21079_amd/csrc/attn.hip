@@ -1,228 +1,205 @@
-// Dense and block-sparse flash attention forward (with LSE) and the block
-// attention-mass search pass, for gfx950.
+// Dense and block-sparse flash attention forward (32 query rows per wave) and
+// the block attention-mass search pass, for gfx950.
 //
-// Orientation.  Every wave owns 32 query rows.  Scores are formed transposed,
-// S^T[key][query] = K Q^T, with K as the MFMA A operand (read from LDS) and the
-// wave's Q fragment as the B operand (kept in registers for the whole loop).
-// In the 32x32 accumulator each lane then holds 16 keys of ONE query, so the
-// softmax row statistics are lane-local plus one exchange between the two
-// half-waves.  The probabilities P^T are already laid out as the B operand of
-// the second product O^T[d][query] += V^T P^T, once the 16 keys of each MFMA
-// step are ordered to match the accumulator rows; the V^T operand is read from
-// a row-major V tile with the LDS transpose read.
-#include "common.hpp"
-#include "launch.hpp"
+// Pipeline.  K/V tiles of 64 keys are double-buffered in LDS and filled by
+// direct global->LDS buffer loads (no register staging); loads for the next
+// tiles are issued before the current tile is computed, so each tile costs one
+// wait and one barrier.  Only a tile that reaches past the end of the sequence
+// pays for key masking.
+#include "attn_tile.hpp"
 
 namespace adaspa {
 
-constexpr int KT = 64;    // keys per tile
-constexpr int PAD = 8;    // bf16 padding per LDS row (16 bytes)
-
-template <int D, int NT>
-struct TileIO {
-  static constexpr int LDR = D + PAD;             // LDS row stride in elements
-  static constexpr int CPR = D / 8;               // 16-byte chunks per row
-  static constexpr int CH = KT * CPR / NT;        // chunks per thread per tile
-  static_assert(KT * CPR % NT == 0, "tile chunks must divide evenly");
-
-  // Global -> registers: rows [kbase, kbase + KT) of a [L, D] matrix; rows at
-  // or beyond L read as zero.
-  __device__ __forceinline__ static void load(const u16* __restrict__ src, int kbase, int L,
-                                              int tid, uint4 (&r)[CH]) {
-#pragma unroll
-    for (int c = 0; c < CH; ++c) {
-      int idx = tid + c * NT;
-      int row = idx / CPR, ch = idx % CPR;
-      int key = kbase + row;
-      if (key < L)
-        r[c] = *reinterpret_cast<const uint4*>(src + (size_t)key * D + ch * 8);
-      else
-        r[c] = make_uint4(0, 0, 0, 0);
-    }
-  }
-  __device__ __forceinline__ static void store(u16* dst, int tid, const uint4 (&r)[CH]) {
-#pragma unroll
-    for (int c = 0; c < CH; ++c) {
-      int idx = tid + c * NT;
-      int row = idx / CPR, ch = idx % CPR;
-      *reinterpret_cast<uint4*>(dst + row * LDR + ch * 8) = r[c];
-    }
-  }
-};
-
-// Key tiles of one workgroup: every tile of the sequence (dense), or the
-// sub-tiles of the key blocks listed in its CSR row (sparse).
-template <bool SPARSE>
-struct TileList {
-  int n = 0;           // number of tiles
-  int start = 0;       // CSR start (sparse)
-  int sub = 1;         // tiles per key block (sparse)
-  int block = 0, nkb = 0, L = 0;
-  const int32_t* cols = nullptr;
-
-  // Key position of tile t, or -1 when the tile holds no valid key.
-  __device__ __forceinline__ int kbase(int t) const {
-    if (!SPARSE) return t * KT;
-    int c = cols[start + t / sub];
-    if (c < 0 || c >= nkb) return -1;
-    int kb = c * block + (t % sub) * KT;
-    return kb < L ? kb : -1;
-  }
-};
-
 // ---------------------------------------------------------------------------
 // Flash attention forward (dense and block-sparse share this body).
+//
+// Full key tiles run through a software pipeline: step t computes the scores
+// of tile t+1 (QK MFMAs) and the output update of tile t-1 (PV MFMAs) while
+// the VALU does the softmax of tile t.  K therefore runs one tile ahead of the
+// scores and V one tile behind; each is double-buffered, with the loads of
+// step t landing in the buffers step t-1 finished reading.  A tile that
+// reaches past the end of the sequence (and, in a malformed sparse row, any
+// out-of-range block) is done afterwards, one at a time with key masking,
+// which keeps the visiting order of the dense and all-blocks sparse paths the
+// same.
 // ---------------------------------------------------------------------------
 template <int D, int NW, bool SPARSE>
 __global__ __launch_bounds__(64 * NW, 2) void attn_fwd_kernel(AttnParams a) {
   constexpr int NT = 64 * NW;
-  using IO = TileIO<D, NT>;
-  constexpr int LDR = IO::LDR;
+  using KDMA = TileDMA<D, NW, 1>;
+  using VDMA = TileDMA<D, NW, 2>;
+  constexpr int KS = KDMA::S, VS = VDMA::S;
   constexpr int ND = D / 32;   // 32-wide output column blocks
   constexpr int NK = D / 16;   // MFMA k-steps over the head dimension
-  __shared__ __attribute__((aligned(16))) u16 sK[KT * LDR];
-  __shared__ __attribute__((aligned(16))) u16 sV[KT * LDR];
+  __shared__ __attribute__((aligned(1024))) u16 sK0[KDMA::ELEMS];
+  __shared__ __attribute__((aligned(1024))) u16 sV0[VDMA::ELEMS];
+  __shared__ __attribute__((aligned(1024))) u16 sK1[KDMA::ELEMS];
+  __shared__ __attribute__((aligned(1024))) u16 sV1[VDMA::ELEMS];
 
-  const int lid = xcd_remap(blockIdx.x, a.n_wg);
-  const int bh = lid / a.nqt;
-  const int qt = lid % a.nqt;
-  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+  int bh, qt;
+  if (a.xcd_map == 2) {
+    xcd_chunk_map(blockIdx.x, a.nqt, a.batch_heads, bh, qt);
+  } else {
+    const int lid = a.xcd_map ? xcd_remap(blockIdx.x, a.n_wg) : (int)blockIdx.x;
+    bh = lid / a.nqt;
+    qt = lid % a.nqt;
+  }
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);   // wave-uniform
   const int hw = lane >> 5, c32 = lane & 31;
+  const int gi = lane & 15, grp = lane >> 4;
   const int L = a.seqlen;
   const size_t hoff = (size_t)bh * L * D;
-  const u16* __restrict__ Kh = a.k + hoff;
-  const u16* __restrict__ Vh = a.v + hoff;
+  const uint32_t hbytes = (uint32_t)L * D * 2u;
+  const __amdgpu_buffer_rsrc_t rK = make_rsrc(a.k + hoff, hbytes);
+  const __amdgpu_buffer_rsrc_t rV = make_rsrc(a.v + hoff, hbytes);
   const int qrow = qt * (32 * NW) + wave * 32 + c32;
+  const int voff = ((4 * hw + (gi >> 2)) * VS) * 8 + 16 * (grp & 1) + 4 * (gi & 3);
+  const int klane = (c32 * KS + hw) * 8;
+
+  // Finite contents everywhere, whatever a bounds-checked load leaves behind.
+  zero_lds<VDMA::SLOTS>(sV0, tid, NT);
+  zero_lds<VDMA::SLOTS>(sV1, tid, NT);
+  zero_lds<KDMA::SLOTS>(sK0, tid, NT);
+  zero_lds<KDMA::SLOTS>(sK1, tid, NT);
 
   bf16x8 qf[NK];
-#pragma unroll
-  for (int ks = 0; ks < NK; ++ks) {
-    if (qrow < L)
-      qf[ks] = *reinterpret_cast<const bf16x8*>(a.q + hoff + (size_t)qrow * D + ks * 16 + hw * 8);
-    else
-      qf[ks] = bf16x8{};
-  }
+  load_q<D>(a.q + hoff, qrow, L, hw, qf);
 
-  TileList<SPARSE> tl;
+  // Tiles: nf full tiles through the pipeline; the rest one by one, masked.
+  int nf = 0;                 // full tiles in the pipeline
+  int e0 = 0, ne = 0;         // sparse: CSR entries [e0, e0 + ne)
+  int skip = -1;              // sparse: entry (relative) holding the ragged block
+  bool slow = false;          // sparse: malformed row, take the masked path for all
+  const int sub = SPARSE ? a.block / KT : 1;
   if constexpr (SPARSE) {
     const int64_t r = (int64_t)bh * a.nkb + qt;
     int64_t s = a.row_ptr[r], e = a.row_ptr[r + 1];
     s = s < 0 ? 0 : (s > a.col_count ? a.col_count : s);
     e = e < s ? s : (e > a.col_count ? a.col_count : e);
-    tl.start = (int)s;
-    tl.sub = a.block / KT;
-    tl.n = (int)(e - s) * tl.sub;
-    tl.block = a.block;
-    tl.nkb = a.nkb;
-    tl.L = L;
-    tl.cols = a.col_idx;
+    e0 = (int)s;
+    ne = (int)(e - s);
+    const bool ragged = L % a.block != 0;
+    for (int i = 0; i < ne; ++i) {
+      const int c = a.col_idx[e0 + i];
+      if (c < 0 || c >= a.nkb) slow = true;
+      else if (ragged && c == a.nkb - 1 && skip < 0) skip = i;
+    }
+    nf = slow ? 0 : (ne - (skip >= 0 ? 1 : 0)) * sub;
   } else {
-    tl.n = (L + KT - 1) / KT;
+    nf = L / KT;
   }
+  auto kbase = [&](int t) -> int {
+    if constexpr (!SPARSE) {
+      return t * KT;
+    } else {
+      int i = t / sub;
+      if (skip >= 0 && i >= skip) ++i;
+      return a.col_idx[e0 + i] * a.block + (t % sub) * KT;
+    }
+  };
 
   const float sl2 = a.scale_log2;
-  float m = -INFINITY, l = 0.f;
+  const float thr = kRescaleLog2 / sl2;   // raw-score margin before the max moves
+  float m = -INFINITY, lsum = 0.f;        // lsum: this lane's half of the row sum
   f32x16 o[ND];
 #pragma unroll
   for (int d = 0; d < ND; ++d) o[d] = f32x16{};
-
-  uint4 rk[IO::CH], rv[IO::CH];
-  int kb_next = tl.n > 0 ? tl.kbase(0) : -1;
-  if (tl.n > 0) {
-    IO::load(Kh, kb_next < 0 ? L : kb_next, L, tid, rk);
-    IO::load(Vh, kb_next < 0 ? L : kb_next, L, tid, rv);
-    IO::store(sK, tid, rk);
-    IO::store(sV, tid, rv);
-  }
   __syncthreads();
 
-  for (int t = 0; t < tl.n; ++t) {
-    const int kb = kb_next;
-    if (t + 1 < tl.n) {
-      kb_next = tl.kbase(t + 1);
-      IO::load(Kh, kb_next < 0 ? L : kb_next, L, tid, rk);
-      IO::load(Vh, kb_next < 0 ? L : kb_next, L, tid, rv);
-    }
+  if (nf > 0) {
+    KDMA::issue(rK, sK0, kbase(0), wave, lane);
+    if (nf > 1) KDMA::issue(rK, sK1, kbase(1), wave, lane);
+    wait_vmem();
+    __syncthreads();
+    f32x16 s_cur[2];
+    qk_tile<D, KS>(sK0, qf, c32, hw, s_cur);
+    __syncthreads();            // sK0 is refilled by step 0
 
-    // S^T = K Q^T for two groups of 32 keys.
+    bf16x8 p_prev[2][2];
+#pragma unroll
+    for (int g = 0; g < 2; ++g)
+#pragma unroll
+      for (int s2 = 0; s2 < 2; ++s2) p_prev[g][s2] = bf16x8{};
+    bool pend = false;
+    float pend_alpha = 1.f;
+
+    // Step t reads K(t+1) and V(t-1) from buffer (t+1)&1 and loads K(t+2),
+    // V(t) into buffer t&1.
+    auto step = [&](int t, const u16* rdK, const u16* rdV, u16* ldK, u16* ldV) {
+      if (pend) {
+#pragma unroll
+        for (int d = 0; d < ND; ++d)
+#pragma unroll
+          for (int e = 0; e < 16; ++e) o[d][e] *= pend_alpha;
+      }
+      if (t + 2 < nf) KDMA::issue(rK, ldK, kbase(t + 2), wave, lane);
+      VDMA::issue(rV, ldV, kbase(t), wave, lane);
+      f32x16 s_next[2];
+      bf16x8 p_cur[2][2];
+      pipelined_step<D, KS, VS>(rdK + klane, rdV + voff, qf, s_cur, p_prev, s_next, p_cur, o, m, lsum,
+                                thr, sl2, pend_alpha, pend);
+#pragma unroll
+      for (int g = 0; g < 2; ++g) {
+        s_cur[g] = s_next[g];
+#pragma unroll
+        for (int s2 = 0; s2 < 2; ++s2) p_prev[g][s2] = p_cur[g][s2];
+      }
+      wait_vmem();
+      __syncthreads();
+    };
+    for (int t = 0; t < nf; t += 2) {
+      step(t, sK1, sV1, sK0, sV0);
+      if (t + 1 < nf) step(t + 1, sK0, sV0, sK1, sV1);
+    }
+    if (pend) {
+#pragma unroll
+      for (int d = 0; d < ND; ++d)
+#pragma unroll
+        for (int e = 0; e < 16; ++e) o[d][e] *= pend_alpha;
+    }
+    pv_tile<ND, VS>(((nf - 1) & 1 ? sV1 : sV0) + voff, p_prev, o);
+    __syncthreads();
+  }
+
+  // Remaining tiles, one at a time with key masking.
+  auto masked_tile = [&](int kb) {
+    KDMA::issue(rK, sK0, kb, wave, lane);
+    VDMA::issue(rV, sV0, kb, wave, lane);
+    wait_vmem();
+    __syncthreads();
     f32x16 s[2];
-#pragma unroll
-    for (int g = 0; g < 2; ++g) {
-      s[g] = f32x16{};
-#pragma unroll
-      for (int ks = 0; ks < NK; ++ks) {
-        bf16x8 kf = *reinterpret_cast<const bf16x8*>(sK + (32 * g + c32) * LDR + ks * 16 + hw * 8);
-        s[g] = mfma32(kf, qf[ks], s[g]);
-      }
-    }
-    const int kvalid = kb < 0 ? 0 : L - kb;
-    if (kvalid < KT) {
-#pragma unroll
-      for (int g = 0; g < 2; ++g)
-#pragma unroll
-        for (int e = 0; e < 16; ++e) {
-          int key = 32 * g + 8 * (e >> 2) + 4 * hw + (e & 3);
-          if (key >= kvalid) s[g][e] = -INFINITY;
-        }
-    }
-
-    // Online softmax (log2 domain).
-    float mt = -INFINITY;
-#pragma unroll
-    for (int g = 0; g < 2; ++g)
-#pragma unroll
-      for (int e = 0; e < 16; ++e) mt = fmaxf(mt, s[g][e]);
-    mt = fmaxf(mt, __shfl_xor(mt, 32, 64));
-    const float mnew = fmaxf(m, mt);
-    const float mc = (mnew == -INFINITY) ? 0.f : mnew * sl2;
-    const float alpha = fast_exp2(m * sl2 - mc);
-    float rs = 0.f;
+    qk_tile<D, KS>(sK0, qf, c32, hw, s);
+    mask_tile(s, L - kb, hw);
     bf16x8 pb[2][2];
+    float alpha;
+    bool moved;
+    softmax_tile(s, m, lsum, thr, sl2, pb, alpha, moved);
+    if (moved) {
 #pragma unroll
-    for (int g = 0; g < 2; ++g)
+      for (int d = 0; d < ND; ++d)
 #pragma unroll
-      for (int e = 0; e < 16; ++e) {
-        float p = fast_exp2(fmaf(s[g][e], sl2, -mc));
-        rs += p;
-        pb[g][e >> 3][e & 7] = (__bf16)p;
+        for (int e = 0; e < 16; ++e) o[d][e] *= alpha;
+    }
+    pv_tile<ND, VS>(sV0 + voff, pb, o);
+    __syncthreads();
+  };
+  if constexpr (SPARSE) {
+    for (int i = 0; i < ne; ++i) {
+      if (!slow && i != skip) continue;
+      const int c = a.col_idx[e0 + i];
+      if (c < 0 || c >= a.nkb) continue;
+      for (int j = 0; j < sub; ++j) {
+        const int kb = c * a.block + j * KT;
+        if (kb < L) masked_tile(kb);
       }
-    l = fmaf(l, alpha, rs);
-    m = mnew;
-#pragma unroll
-    for (int d = 0; d < ND; ++d)
-#pragma unroll
-      for (int e = 0; e < 16; ++e) o[d][e] *= alpha;
-
-    // O^T += V^T P^T.  MFMA step (g, s2) covers keys 32g + 16s2 + 8u + 4hw + j
-    // (u, j in 0..1, 0..3); lane (hw, e) supplies key index 8*(e/4) + 4*hw + e%4.
-    const int gi = lane & 15, grp = lane >> 4;
-#pragma unroll
-    for (int d = 0; d < ND; ++d) {
-      const int dcol = d * 32 + 16 * (grp & 1) + 4 * (gi & 3);
-#pragma unroll
-      for (int g = 0; g < 2; ++g)
-#pragma unroll
-        for (int s2 = 0; s2 < 2; ++s2) {
-          const u16* p0 = sV + (32 * g + 16 * s2 + 4 * hw + (gi >> 2)) * LDR + dcol;
-          s16x4 lo = lds_read_tr16(p0);
-          s16x4 hi = lds_read_tr16(p0 + 8 * LDR);
-          bf16x8 vf;
-          __builtin_memcpy(&vf, &lo, 8);
-          __builtin_memcpy(reinterpret_cast<char*>(&vf) + 8, &hi, 8);
-          o[d] = mfma32(vf, pb[g][s2], o[d]);
-        }
     }
-
-    __syncthreads();
-    if (t + 1 < tl.n) {
-      IO::store(sK, tid, rk);
-      IO::store(sV, tid, rv);
-    }
-    __syncthreads();
+  } else {
+    if (nf * KT < L) masked_tile(nf * KT);
   }
 
   // Normalise and store.
-  const float lt = l + __shfl_xor(l, 32, 64);
+  const float lt = lsum + __shfl_xor(lsum, 32, 64);
   const float inv = lt > 0.f ? 1.f / lt : 0.f;
   if (qrow < L) {
     u16* orow = a.o + hoff + (size_t)qrow * D;
@@ -246,87 +223,96 @@ __global__ __launch_bounds__(64 * NW, 2) void attn_fwd_kernel(AttnParams a) {
 template <int D, int NW>
 __global__ __launch_bounds__(64 * NW, 2) void block_mass_kernel(MassParams a) {
   constexpr int NT = 64 * NW;
-  using IO = TileIO<D, NT>;
-  constexpr int LDR = IO::LDR;
+  using KDMA = TileDMA<D, NW, 1>;
+  constexpr int KS = KDMA::S;
   constexpr int NK = D / 16;
-  __shared__ __attribute__((aligned(16))) u16 sK[KT * LDR];
-  __shared__ float sRed[NW];        // per-wave sums of the block just finished
+  __shared__ __attribute__((aligned(1024))) u16 sK0[KDMA::ELEMS];
+  __shared__ __attribute__((aligned(1024))) u16 sK1[KDMA::ELEMS];
+  __shared__ float sRed[2][NW];     // per-wave sums of the last two blocks
 
-  const int lid = xcd_remap(blockIdx.x, a.n_wg);
-  const int bh = lid / a.nkb;
-  const int p = lid % a.nkb;
-  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+  int bh, p;
+  if (a.xcd_map == 2) {
+    xcd_chunk_map(blockIdx.x, a.nkb, a.batch_heads, bh, p);
+  } else {
+    const int lid = a.xcd_map ? xcd_remap(blockIdx.x, a.n_wg) : (int)blockIdx.x;
+    bh = lid / a.nkb;
+    p = lid % a.nkb;
+  }
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);   // wave-uniform
   const int hw = lane >> 5, c32 = lane & 31;
   const int L = a.seqlen;
   const size_t hoff = (size_t)bh * L * D;
-  const u16* __restrict__ Kh = a.k + hoff;
+  const __amdgpu_buffer_rsrc_t rK = make_rsrc(a.k + hoff, (uint32_t)L * D * 2u);
   const int qrow = p * a.block + wave * 32 + c32;   // block = 32 * NW
   const bool qvalid = qrow < L;
 
+  zero_lds<KDMA::SLOTS>(sK0, tid, NT);
+  zero_lds<KDMA::SLOTS>(sK1, tid, NT);
   bf16x8 qf[NK];
-#pragma unroll
-  for (int ks = 0; ks < NK; ++ks) {
-    if (qvalid)
-      qf[ks] = *reinterpret_cast<const bf16x8*>(a.q + hoff + (size_t)qrow * D + ks * 16 + hw * 8);
-    else
-      qf[ks] = bf16x8{};
-  }
+  load_q<D>(a.q + hoff, qrow, L, hw, qf);
   const float lse2 = qvalid ? a.lse[(size_t)bh * L + qrow] * kLog2e : INFINITY;
   const float sl2 = a.scale_log2;
   const int sub = a.block / KT;
   const int ntile = a.nkb * sub;
+  float* wrow = a.w + ((size_t)bh * a.nkb + p) * a.nkb;
 
-  uint4 rk[IO::CH];
-  IO::load(Kh, 0, L, tid, rk);
-  IO::store(sK, tid, rk);
+  __syncthreads();
+  if (L >= KT) KDMA::issue(rK, sK0, 0, wave, lane);
+  wait_vmem();
   __syncthreads();
 
-  float* wrow = a.w + ((size_t)bh * a.nkb + p) * a.nkb;
   float acc = 0.f;
-  for (int t = 0; t < ntile; ++t) {
-    const int kb = t * KT;
-    if (t + 1 < ntile) IO::load(Kh, kb + KT, L, tid, rk);
+  auto tile = [&](auto masked, const u16* cK, int kb) {
     f32x16 s[2];
-#pragma unroll
-    for (int g = 0; g < 2; ++g) {
-      s[g] = f32x16{};
-#pragma unroll
-      for (int ks = 0; ks < NK; ++ks) {
-        bf16x8 kf = *reinterpret_cast<const bf16x8*>(sK + (32 * g + c32) * LDR + ks * 16 + hw * 8);
-        s[g] = mfma32(kf, qf[ks], s[g]);
-      }
-    }
-    const int kvalid = L - kb;
-    if (kvalid < KT) {
-#pragma unroll
-      for (int g = 0; g < 2; ++g)
-#pragma unroll
-        for (int e = 0; e < 16; ++e) {
-          int key = 32 * g + 8 * (e >> 2) + 4 * hw + (e & 3);
-          if (key >= kvalid) s[g][e] = -INFINITY;
-        }
-    }
+    qk_tile<D, KS>(cK, qf, c32, hw, s);
+    if constexpr (decltype(masked)::value) mask_tile(s, L - kb, hw);
 #pragma unroll
     for (int g = 0; g < 2; ++g)
 #pragma unroll
       for (int e = 0; e < 16; ++e) acc += fast_exp2(fmaf(s[g][e], sl2, -lse2));
-
-    const bool block_end = (t + 1) % sub == 0;
-    if (block_end) {
-      float w = wave_sum(acc);
-      if (lane == 0) sRed[wave] = w;
-      acc = 0.f;
-    }
-    __syncthreads();
+  };
+  // Full tiles in the loop; a block whose last tile is ragged (or missing)
+  // is finished after it, with the masked tile.
+  const int nfull = L / KT;
+  auto finish_block = [&](int blk) {
+    const float w = wave_sum(acc);
+    if (lane == 0) sRed[blk & 1][wave] = w;
+    acc = 0.f;
+  };
+  auto publish = [&](int blk) {
     // Waves are combined in a fixed order, so the result is deterministic.
-    if (block_end && tid == 0) {
+    if (tid == 0) {
       float v = 0.f;
 #pragma unroll
-      for (int w = 0; w < NW; ++w) v += sRed[w];
-      wrow[t / sub] = v;
+      for (int w = 0; w < NW; ++w) v += sRed[blk & 1][w];
+      wrow[blk] = v;
     }
-    if (t + 1 < ntile) IO::store(sK, tid, rk);
+  };
+  auto step = [&](int t, const u16* cK, u16* nK) {
+    const int kb = t * KT;
+    if (t + 1 < nfull) KDMA::issue(rK, nK, kb + KT, wave, lane);
+    tile(std::false_type{}, cK, kb);
+    const bool block_end = (t + 1) % sub == 0;
+    if (block_end) finish_block(t / sub);
+    wait_vmem();
     __syncthreads();
+    if (block_end) publish(t / sub);
+  };
+  for (int t = 0; t < nfull; t += 2) {
+    step(t, sK0, sK1);
+    if (t + 1 < nfull) step(t + 1, sK1, sK0);
+  }
+  if (nfull < ntile && nfull * KT < L) {
+    KDMA::issue(rK, sK0, nfull * KT, wave, lane);
+    wait_vmem();
+    __syncthreads();
+    tile(std::true_type{}, sK0, nfull * KT);
+  }
+  if (nfull % sub != 0 || nfull * KT < L) {
+    finish_block(a.nkb - 1);
+    __syncthreads();
+    publish(a.nkb - 1);
   }
 }
 
@@ -340,7 +326,9 @@ static hipError_t launch_attn(const AttnParams& a, hipStream_t st) {
 }
 
 hipError_t launch_dense(AttnParams a, int D, hipStream_t st) {
-  // 128 query rows per workgroup.
+  // 128 query rows per workgroup (four waves of 32 rows).
+  a.row_ptr = nullptr;
+  a.col_idx = nullptr;
   a.nqt = (a.seqlen + 127) / 128;
   a.n_wg = a.nqt * a.batch_heads;
   if (D == 64) return launch_attn<64, 4, false>(a, st);

@@ -44,6 +44,30 @@ __device__ __forceinline__ int xcd_remap(int bid, int n) {
   return off + k;
 }
 
+// Head-chunked mapping: each head's nqt tiles are cut into 8 contiguous
+// chunks and XCD x runs chunk x of every head, so every XCD works on a
+// contiguous run of query tiles (its L2 keeps the shared K/V) and on an equal
+// share of every head (heads of different cost stay balanced).  Tiles are
+// ordered (chunk, head, tile) and the round-robin dispatch share of XCD x is
+// a contiguous segment of that order, so the map is a bijection for any sizes.
+__device__ __forceinline__ void xcd_chunk_map(int bid, int nqt, int nbh, int& bh, int& qt) {
+  const int nx = 8, n = nqt * nbh;
+  const int q = n / nx, r = n % nx;
+  const int x = bid % nx, k = bid / nx;
+  const int idx = x * q + (x < r ? x : r) + k;        // position in (chunk, head, tile) order
+  // chunk c covers tiles [c*nqt/8, (c+1)*nqt/8) of every head
+  int c = 0, start = 0;
+  for (; c < nx - 1; ++c) {
+    const int sz = ((c + 1) * nqt) / nx - (c * nqt) / nx;
+    if (idx < start + sz * nbh) break;
+    start += sz * nbh;
+  }
+  const int c0 = (c * nqt) / nx, sz = ((c + 1) * nqt) / nx - c0;
+  const int rel = idx - start;
+  bh = rel / sz;
+  qt = c0 + rel % sz;
+}
+
 __device__ __forceinline__ float wave_sum(float v) {
 #pragma unroll
   for (int o = 32; o >= 1; o >>= 1) v += __shfl_xor(v, o, 64);

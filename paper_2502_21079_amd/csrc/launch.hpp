@@ -25,6 +25,7 @@ struct AttnParams {
   int n_wg;                   // workgroups (set by the launcher)
   float scale;
   float scale_log2;           // scale * log2(e)
+  int xcd_map;                // 0 hardware order, 1 contiguous per XCD, 2 head-chunked
 };
 
 struct MassParams {
@@ -38,6 +39,7 @@ struct MassParams {
   int nkb;
   int n_wg;
   float scale_log2;
+  int xcd_map;
 };
 
 constexpr int kMaxHeads = 512;
@@ -69,5 +71,9 @@ hipError_t launch_dense(AttnParams a, int head_dim, hipStream_t st);
 hipError_t launch_sparse(AttnParams a, int head_dim, hipStream_t st);
 hipError_t launch_block_mass(MassParams a, int head_dim, hipStream_t st);
 hipError_t launch_select(const SelectParams& p, hipStream_t st);
+
+// Work-to-XCD mapping for the attention and mass kernels (0 hardware order,
+// 1 contiguous per XCD, 2 head-chunked); kernel_default unless overridden.
+int xcd_map_mode(int kernel_default);
 
 }  // namespace adaspa
