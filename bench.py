@@ -17,8 +17,8 @@ a bounded sample on this host.
 from __future__ import annotations
 
 import argparse
+import hashlib
 import json
-import math
 import os
 import sys
 import time
@@ -34,6 +34,23 @@ from workloads import LONG, make_qkv  # noqa: E402
 
 PEAK_BF16_TFLOPS = 2500.0     # MI355X dense bf16 MFMA
 PEAK_HBM_GBS = 8000.0
+
+
+def measured_traffic(kind: str):
+    """HBM bytes per launch of a kernel from the committed rocprofv3 record
+    (FETCH_SIZE and WRITE_SIZE, scaled by a plain-copy calibration), or None
+    when the kernel sources changed since the counters were taken."""
+    path = os.path.join(ROOT, "profiles", "hbm_traffic.json")
+    try:
+        rec = json.load(open(path))
+        h = hashlib.sha256()
+        for f in rec["sources"]:
+            h.update(open(os.path.join(ROOT, f), "rb").read())
+        if h.hexdigest()[:16] != rec["source_sha256_16"]:
+            return None
+        return rec["kernels"][kind]["total_bytes"]
+    except (OSError, KeyError, ValueError):
+        return None
 
 
 def attn_flops(L: int, D: int, H: int, B: int = 1) -> float:
@@ -253,10 +270,19 @@ def main():
         print("[bench] cpu oracle baseline", file=sys.stderr, flush=True)
         cpu = cpu_oracle_baseline(q, k, v, w, args.cpu_budget)
 
+    # The dominant kernel of a step is the dense pass; the block-sparse pass
+    # (the metric's kernel) gets the same record beside it.
     roof = {"kernel": "dense_attn_lse", "bound": "mfma", "achieved": round(tf(f_dense, dense_ms), 1),
             "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
-            "frac": round(tf(f_dense, dense_ms) / PEAK_BF16_TFLOPS, 4), "traffic": None,
+            "frac": round(tf(f_dense, dense_ms) / PEAK_BF16_TFLOPS, 4),
+            "traffic": measured_traffic("dense"),
             "algorithmic_flops_per_launch": f_dense}
+    roof_sparse = None
+    if "keep20" in sweep:
+        s20 = sweep["keep20"]
+        roof_sparse = {"kernel": "block_sparse_attn (keep 20%)", "bound": "mfma",
+                       "achieved": s20["tflops"], "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
+                       "frac": s20["frac_bf16_peak"], "traffic": measured_traffic("sparse")}
     line = {
         "metric": "block-sparse attn ms + effective TFLOP/s @110K tok,24h,d128; search ms vs dense",
         "value": round(tf(f_sparse, sparse_ms), 2),
@@ -272,7 +298,7 @@ def main():
         "sparse_ms": round(sparse_ms, 3), "dense_ms": round(dense_ms, 3), "search_ms": round(search_ms, 3),
         "search_vs_dense": round(search_ms / dense_ms, 4),
         "kernels": kernels, "density_sweep": sweep, "detail": detail,
-        "roofline": roof, "cpu_baseline": cpu,
+        "roofline": roof, "roofline_sparse_keep20": roof_sparse, "cpu_baseline": cpu,
     }
     print(json.dumps(line), flush=True)
 
