@@ -30,7 +30,7 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 import paper_2502_21079_amd as ad  # noqa: E402
-from workloads import LONG, make_qkv  # noqa: E402
+from workloads import LONG, make_drift_noise, make_qkv  # noqa: E402
 
 PEAK_BF16_TFLOPS = 2500.0     # MI355X dense bf16 MFMA
 PEAK_HBM_GBS = 8000.0
@@ -130,6 +130,60 @@ def cpu_oracle_baseline(q, k, v, w, budget_s: float):
             "total_wall_s": round(time.perf_counter() - t0, 1)}
 
 
+def amortised_loop(w, tau, steps: int = 50, drift: float = 0.05):
+    """The denoising-loop workload: X_t = X_0 + (drift * t / steps) * E for
+    t = 0 .. steps-1 with one fixed N(0,1) draw E per tensor.  Step 0 runs
+    dense attention + LSE and the block search; steps 1.. reuse the step-0
+    block pattern in block-sparse attention.  Every step's dense attention is
+    also computed, untimed, as the reference for that step's error."""
+    B, H, L, D, blk = w.batch, w.heads, w.seqlen, w.head_dim, w.block
+    x0 = make_qkv(w, device="cuda", fp32=True)
+    eps = make_drift_noise(w, device="cuda", seed=4)
+    xt = [torch.empty(B, H, L, D, dtype=torch.bfloat16, device="cuda") for _ in range(3)]
+    dense_out = torch.empty_like(xt[0])
+    sp_out = torch.empty_like(xt[0])
+    lse = torch.empty(B, H, L, dtype=torch.float32, device="cuda")
+    wsb = ad.block_search_workspace((B, H, L, D), blk, w.text_start, w.text_len, "coverage", tau)
+    ws = torch.empty(wsb, dtype=torch.uint8, device="cuda")
+    timer = Timer()
+    res = None
+    per_step = []
+    for t in range(steps):
+        c = drift * t / steps
+        for i in range(3):
+            xt[i].copy_(torch.add(x0[i], eps[i], alpha=c))     # rounded to bf16
+        q, k, v = xt
+        if t == 0:
+            timer("dense", ad.dense_attn_lse, q, k, v, out=dense_out, lse=lse)
+            res = timer("search", ad.block_search, q, k, lse, block=blk, text_start=w.text_start,
+                        text_len=w.text_len, mode="coverage", head_param_bp=tau, workspace=ws)
+            per_step.append({"t": 0, "path": "dense"})
+            continue
+        timer("sparse", ad.block_sparse_attn, q, k, v, res.row_ptr, res.col_idx, block=blk,
+              out=sp_out, want_lse=False)
+        ad.dense_attn_lse(q, k, v, out=dense_out, want_lse=False)     # reference, untimed
+        d = (sp_out.float() - dense_out.float())
+        rel = (d.norm() / dense_out.float().norm()).item()
+        per_step.append({"t": t, "max_abs": round(d.abs().max().item(), 5),
+                         "mean_abs": round(d.abs().mean().item(), 6), "rel_l2": round(rel, 6)})
+        del d
+    ev = timer.collect()
+    dense_ms, search_ms = ev["dense"][0], ev["search"][0]
+    sparse_ms = float(np.sum(ev["sparse"]))
+    total = dense_ms + search_ms + sparse_ms
+    errs = per_step[1:]
+    return {"steps": steps, "attention_ms_total": round(total, 3),
+            "dense_ms_step0": round(dense_ms, 3), "search_ms_step0": round(search_ms, 3),
+            "sparse_ms_mean": round(sparse_ms / (steps - 1), 3),
+            "all_dense_ms_estimate": round(steps * dense_ms, 3),
+            "speedup_vs_all_dense": round(steps * dense_ms / total, 3),
+            "density": round(res.nnz() / (B * H * w.nblocks ** 2), 5),
+            "error_vs_dense_last_step": errs[-1], "error_vs_dense_max_over_steps": {
+                "max_abs": max(e["max_abs"] for e in errs), "mean_abs": max(e["mean_abs"] for e in errs),
+                "rel_l2": max(e["rel_l2"] for e in errs)},
+            "per_step": per_step}
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -142,6 +196,8 @@ def main():
                     help="with --kernel sparse: per-head keep fraction (basis points, TOPK) "
                          "instead of the coverage selection")
     ap.add_argument("--no-cpu", action="store_true")
+    ap.add_argument("--no-amortised", action="store_true",
+                    help="skip the 50-step denoising-loop workload")
     ap.add_argument("--kernel", choices=["all", "dense", "sparse", "search", "copy"], default="all",
                     help="profile helper: run only one kernel in the timed loop; 'copy' runs a "
                          "plain 1 GiB device copy, the reference for HBM byte counters")
@@ -265,6 +321,13 @@ def main():
                            "speedup_vs_dense": round(dense_ms / ms, 3),
                            "head_imbalance": round(float(hk.max() / hk.mean()), 3)}
 
+    amort = None
+    if not args.no_amortised and not args.no_sweep:
+        print("[bench] amortised 50-step loop", file=sys.stderr, flush=True)
+        del ws
+        torch.cuda.empty_cache()
+        amort = amortised_loop(w, tau)
+
     cpu = None
     if not args.no_cpu:
         print("[bench] cpu oracle baseline", file=sys.stderr, flush=True)
@@ -297,7 +360,7 @@ def main():
                    "step": "dense_attn_lse -> block_search -> block_sparse_attn"},
         "sparse_ms": round(sparse_ms, 3), "dense_ms": round(dense_ms, 3), "search_ms": round(search_ms, 3),
         "search_vs_dense": round(search_ms / dense_ms, 4),
-        "kernels": kernels, "density_sweep": sweep, "detail": detail,
+        "kernels": kernels, "density_sweep": sweep, "amortised_loop": amort, "detail": detail,
         "roofline": roof, "roofline_sparse_keep20": roof_sparse, "cpu_baseline": cpu,
     }
     print(json.dumps(line), flush=True)
