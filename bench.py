@@ -130,12 +130,24 @@ def cpu_oracle_baseline(q, k, v, w, budget_s: float):
             "total_wall_s": round(time.perf_counter() - t0, 1)}
 
 
-def amortised_loop(w, tau, steps: int = 50, drift: float = 0.05):
+def err_stats(got, ref):
+    d = got.float() - ref.float()
+    rel = (d.norm() / ref.float().norm()).item()
+    return {"max_abs": round(d.abs().max().item(), 5), "mean_abs": round(d.abs().mean().item(), 6),
+            "rel_l2": round(rel, 6)}
+
+
+def amortised_loop(w, tau, steps: int = 50, drift: float = 0.05, research_at: int = 30):
     """The denoising-loop workload: X_t = X_0 + (drift * t / steps) * E for
     t = 0 .. steps-1 with one fixed N(0,1) draw E per tensor.  Step 0 runs
     dense attention + LSE and the block search; steps 1.. reuse the step-0
     block pattern in block-sparse attention.  Every step's dense attention is
-    also computed, untimed, as the reference for that step's error."""
+    also computed, untimed, as the reference for that step's error.
+
+    Beside it runs the two-phase schedule of the paper's overview (Fig. 6):
+    at step ``research_at`` the search is repeated with the LSE cached at step
+    0 (Algorithm 2, no dense pass) and later steps use the new pattern; its
+    per-step error is reported for those steps."""
     B, H, L, D, blk = w.batch, w.heads, w.seqlen, w.head_dim, w.block
     x0 = make_qkv(w, device="cuda", fp32=True)
     eps = make_drift_noise(w, device="cuda", seed=4)
@@ -162,16 +174,34 @@ def amortised_loop(w, tau, steps: int = 50, drift: float = 0.05):
         timer("sparse", ad.block_sparse_attn, q, k, v, res.row_ptr, res.col_idx, block=blk,
               out=sp_out, want_lse=False)
         ad.dense_attn_lse(q, k, v, out=dense_out, want_lse=False)     # reference, untimed
-        d = (sp_out.float() - dense_out.float())
-        rel = (d.norm() / dense_out.float().norm()).item()
-        per_step.append({"t": t, "max_abs": round(d.abs().max().item(), 5),
-                         "mean_abs": round(d.abs().mean().item(), 6), "rel_l2": round(rel, 6)})
-        del d
+        rec = {"t": t, **err_stats(sp_out, dense_out)}
+        if t == research_at:
+            res2 = timer("search_cached_lse", ad.block_search, q, k, lse, block=blk,
+                         text_start=w.text_start, text_len=w.text_len, mode="coverage",
+                         head_param_bp=tau)
+        if t >= research_at:
+            timer("sparse_phase2", ad.block_sparse_attn, q, k, v, res2.row_ptr, res2.col_idx,
+                  block=blk, out=sp_out, want_lse=False)
+            rec["two_phase"] = err_stats(sp_out, dense_out)
+        per_step.append(rec)
     ev = timer.collect()
     dense_ms, search_ms = ev["dense"][0], ev["search"][0]
     sparse_ms = float(np.sum(ev["sparse"]))
     total = dense_ms + search_ms + sparse_ms
     errs = per_step[1:]
+    late = [e for e in errs if "two_phase" in e]
+    two_phase = {
+        "research_step": research_at,
+        "search_cached_lse_ms": round(ev["search_cached_lse"][0], 3),
+        "fused_search_ms_step0": round(dense_ms + search_ms, 3),
+        "density_phase2": round(res2.nnz() / (B * H * w.nblocks ** 2), 5),
+        "head_recall_phase2_mean": float(res2.head_recall.float().mean().item()),
+        "rel_l2_late_steps_single_search": round(float(np.mean([e["rel_l2"] for e in late])), 6),
+        "rel_l2_late_steps_two_phase": round(float(np.mean([e["two_phase"]["rel_l2"] for e in late])), 6),
+        "attention_ms_total": round(dense_ms + search_ms + ev["search_cached_lse"][0]
+                                    + float(np.sum(ev["sparse"][:research_at - 1]))
+                                    + float(np.sum(ev["sparse_phase2"])), 3),
+    }
     return {"steps": steps, "attention_ms_total": round(total, 3),
             "dense_ms_step0": round(dense_ms, 3), "search_ms_step0": round(search_ms, 3),
             "sparse_ms_mean": round(sparse_ms / (steps - 1), 3),
@@ -181,7 +211,7 @@ def amortised_loop(w, tau, steps: int = 50, drift: float = 0.05):
             "error_vs_dense_last_step": errs[-1], "error_vs_dense_max_over_steps": {
                 "max_abs": max(e["max_abs"] for e in errs), "mean_abs": max(e["mean_abs"] for e in errs),
                 "rel_l2": max(e["rel_l2"] for e in errs)},
-            "per_step": per_step}
+            "two_phase_schedule": two_phase, "per_step": per_step}
 
 
 def main():

@@ -78,7 +78,15 @@ enum {
   ADASPA_SELECT_TOPK = 0,
   /* k_h = smallest count whose head Recall (Sec. 2.3, text rows counted as
    * fully kept) reaches head_param_bp[h] / 10000. */
-  ADASPA_SELECT_COVERAGE = 1
+  ADASPA_SELECT_COVERAGE = 1,
+  /* Head-adaptive hierarchical sparsity (Sec. 4.2).  At base sparsity s
+   * (base_sparsity_bp) every head keeps k(s) blocks per row; n = number of
+   * heads whose Recall there exceeds recall_threshold_bp (strictly), capped at
+   * floor(H/2).  The n heads of highest Recall (ties: lower head index) move
+   * to sparsity (1+s)/2, the n of lowest Recall to (3s-1)/2 (at least 0);
+   * k(x) is the TOPK count of keep fraction 1-x.  Heads are ranked within each
+   * batch element; Recall is compared exactly.  head_param_bp is unused. */
+  ADASPA_SELECT_HIERARCHICAL = 2
 };
 
 /* Flags */
@@ -92,7 +100,10 @@ typedef struct {
   int32_t flags;                /* ADASPA_F_*                                     */
   const int32_t* head_param_bp; /* HOST array [H]: keep fraction (TOPK) or Recall
                                    target (COVERAGE) in basis points, 0..10000;
-                                   applies to every batch element               */
+                                   applies to every batch element; may be NULL
+                                   for HIERARCHICAL                              */
+  int32_t base_sparsity_bp;     /* HIERARCHICAL: base sparsity s, 0..10000        */
+  int32_t recall_threshold_bp;  /* HIERARCHICAL: Recall threshold, 0..10000       */
 } adaspa_select;
 
 /* Human-readable name of a status code (static storage). */
@@ -112,8 +123,10 @@ size_t adaspa_block_search_workspace(const adaspa_problem* prob,
                                      const adaspa_select* sel);
 
 /* Number of col_idx entries the selection may write: the exact count for
- * TOPK, B*H*NB*NB for COVERAGE (the count depends on the data and the library
- * never synchronises to learn it).  Returns -1 for invalid arguments. */
+ * TOPK, an upper bound for HIERARCHICAL (every head at the largest of its
+ * three counts), B*H*NB*NB for COVERAGE (the counts depend on the data and
+ * the library never synchronises to learn them).  Returns -1 for invalid
+ * arguments. */
 int64_t adaspa_block_search_capacity(const adaspa_problem* prob,
                                      const adaspa_select* sel);
 

@@ -35,6 +35,7 @@ EXPORTED_SYMBOLS = ("adaspa_status_string", "adaspa_dense_attn_lse",
 
 SELECT_TOPK = 0
 SELECT_COVERAGE = 1
+SELECT_HIERARCHICAL = 2
 F_TEXT_SINK = 1
 F_SCORES_GIVEN = 2
 
@@ -52,7 +53,8 @@ class _Problem(ctypes.Structure):
 
 class _Select(ctypes.Structure):
     _fields_ = [("mode", ctypes.c_int32), ("flags", ctypes.c_int32),
-                ("head_param_bp", ctypes.POINTER(ctypes.c_int32))]
+                ("head_param_bp", ctypes.POINTER(ctypes.c_int32)),
+                ("base_sparsity_bp", ctypes.c_int32), ("recall_threshold_bp", ctypes.c_int32)]
 
 
 _lib = None
@@ -124,11 +126,14 @@ def _check_qkv(*ts):
             raise AdaspaError(f"shape mismatch {tuple(t.shape)} vs {tuple(ref.shape)}")
 
 
-def _select(mode: str, head_param_bp: Sequence[int], text_sink: bool, scores_given: bool):
-    m = {"topk": SELECT_TOPK, "coverage": SELECT_COVERAGE}[mode]
-    arr = (ctypes.c_int32 * len(head_param_bp))(*[int(x) for x in head_param_bp])
+def _select(mode: str, head_param_bp: Optional[Sequence[int]], text_sink: bool,
+            scores_given: bool, base_sparsity_bp: int = 8000, recall_threshold_bp: int = 8000):
+    m = {"topk": SELECT_TOPK, "coverage": SELECT_COVERAGE, "hierarchical": SELECT_HIERARCHICAL}[mode]
+    params = list(head_param_bp) if head_param_bp is not None else []
+    arr = (ctypes.c_int32 * max(1, len(params)))(*[int(x) for x in params])
+    ptr = ctypes.cast(arr, ctypes.POINTER(ctypes.c_int32)) if params else None
     flags = (F_TEXT_SINK if text_sink else 0) | (F_SCORES_GIVEN if scores_given else 0)
-    return _Select(m, flags, ctypes.cast(arr, ctypes.POINTER(ctypes.c_int32))), arr
+    return _Select(m, flags, ptr, int(base_sparsity_bp), int(recall_threshold_bp)), arr
 
 
 def dense_attn_lse(q, k, v, *, scale: Optional[float] = None, out=None, lse=None,
@@ -180,13 +185,16 @@ def block_search_capacity(shape, block, text_start, text_len, mode, head_param_b
 
 
 def block_search(q, k, lse, *, block: int, text_start: int, text_len: int,
-                 mode: str, head_param_bp: Sequence[int], text_sink: bool = True,
+                 mode: str, head_param_bp: Optional[Sequence[int]] = None, text_sink: bool = True,
                  scale: Optional[float] = None, scores: Optional[torch.Tensor] = None,
-                 shape=None, workspace: Optional[torch.Tensor] = None) -> SearchResult:
+                 shape=None, workspace: Optional[torch.Tensor] = None,
+                 base_sparsity_bp: int = 8000, recall_threshold_bp: int = 8000) -> SearchResult:
     """Block masses W_sum_attn from ``lse`` (fresh or cached) and the per-head
-    selection.  With ``scores`` given (fp32 [B, H, NB, NB]) the mass pass is
-    skipped and those masses are selected from (then q, k, lse may be None and
-    ``shape`` = (B, H, L, D) is required)."""
+    selection.  ``mode`` is "topk" or "coverage" (per-head ``head_param_bp``)
+    or "hierarchical" (``base_sparsity_bp``, ``recall_threshold_bp``, Sec. 4.2).
+    With ``scores`` given (fp32 [B, H, NB, NB]) the mass pass is skipped and
+    those masses are selected from (then q, k, lse may be None and ``shape`` =
+    (B, H, L, D) is required)."""
     lib = load_library()
     given = scores is not None
     if given:
@@ -200,7 +208,8 @@ def block_search(q, k, lse, *, block: int, text_start: int, text_len: int,
             raise AdaspaError("lse must be contiguous fp32 [B, H, L]")
     nb = (L + block - 1) // block
     prob = _problem_shape(B, H, L, D, block, text_start, text_len, scale)
-    sel, _keep = _select(mode, head_param_bp, text_sink, given)
+    sel, _keep = _select(mode, head_param_bp, text_sink, given, base_sparsity_bp,
+                         recall_threshold_bp)
     cap = lib.adaspa_block_search_capacity(ctypes.byref(prob), ctypes.byref(sel))
     wsb = lib.adaspa_block_search_workspace(ctypes.byref(prob), ctypes.byref(sel))
     if cap < 0 or wsb == 0:

@@ -52,13 +52,22 @@ void text_block_range(const adaspa_problem* p, bool sink, int* lo, int* hi) {
 }
 
 adaspa_status check_select(const adaspa_problem* p, const adaspa_select* s) {
-  if (!s || !s->head_param_bp) return ADASPA_ERR_INVALID_ARG;
-  if (s->mode != ADASPA_SELECT_TOPK && s->mode != ADASPA_SELECT_COVERAGE) return ADASPA_ERR_UNSUPPORTED;
+  if (!s) return ADASPA_ERR_INVALID_ARG;
+  if (s->mode != ADASPA_SELECT_TOPK && s->mode != ADASPA_SELECT_COVERAGE &&
+      s->mode != ADASPA_SELECT_HIERARCHICAL)
+    return ADASPA_ERR_UNSUPPORTED;
   if (s->flags & ~(ADASPA_F_TEXT_SINK | ADASPA_F_SCORES_GIVEN)) return ADASPA_ERR_INVALID_ARG;
   if (p->heads > kMaxHeads) return ADASPA_ERR_UNSUPPORTED;
   if (num_blocks(p) > kMaxBlocks) return ADASPA_ERR_UNSUPPORTED;
-  for (int h = 0; h < p->heads; ++h)
-    if (s->head_param_bp[h] < 0 || s->head_param_bp[h] > 10000) return ADASPA_ERR_INVALID_ARG;
+  if (s->mode == ADASPA_SELECT_HIERARCHICAL) {
+    if (s->base_sparsity_bp < 0 || s->base_sparsity_bp > 10000 || s->recall_threshold_bp < 0 ||
+        s->recall_threshold_bp > 10000)
+      return ADASPA_ERR_INVALID_ARG;
+  } else {
+    if (!s->head_param_bp) return ADASPA_ERR_INVALID_ARG;
+    for (int h = 0; h < p->heads; ++h)
+      if (s->head_param_bp[h] < 0 || s->head_param_bp[h] > 10000) return ADASPA_ERR_INVALID_ARG;
+  }
   // Entries of col_idx / row_ptr are int32.
   int64_t nb = num_blocks(p);
   if ((int64_t)p->batch * p->heads * nb * nb >= ((int64_t)1 << 31)) return ADASPA_ERR_UNSUPPORTED;
@@ -90,6 +99,17 @@ int topk_count(int keep_bp, int nb, int n_text) {
   if (k > nb) k = nb;
   if (k < kmin) k = kmin;
   return (int)k;
+}
+
+// Counts of the hierarchical mode (Sec. 4.2) at sparsity s, (1+s)/2 and
+// (3s-1)/2 (at least 0), all in basis points.
+void hierarchical_counts(int s_bp, int nb, int n_text, int* k_base, int* k_hi, int* k_lo) {
+  const int s_hi = (10000 + s_bp) / 2;
+  const int s_lo3 = 3 * s_bp - 10000;
+  const int s_lo = s_lo3 > 0 ? s_lo3 / 2 : 0;
+  *k_base = topk_count(10000 - s_bp, nb, n_text);
+  *k_hi = topk_count(10000 - s_hi, nb, n_text);
+  *k_lo = topk_count(10000 - s_lo, nb, n_text);
 }
 
 }  // namespace
@@ -163,6 +183,13 @@ int64_t adaspa_block_search_capacity(const adaspa_problem* prob, const adaspa_se
   int lo, hi;
   text_block_range(prob, (sel->flags & ADASPA_F_TEXT_SINK) != 0, &lo, &hi);
   const int n_text = lo <= hi ? hi - lo + 1 : 0;
+  if (sel->mode == ADASPA_SELECT_HIERARCHICAL) {
+    int kb, kh, kl;
+    hierarchical_counts(sel->base_sparsity_bp, (int)nb, n_text, &kb, &kh, &kl);
+    int kmax = kb > kh ? kb : kh;
+    kmax = kmax > kl ? kmax : kl;
+    return bh * (n_text * nb + (nb - n_text) * kmax);
+  }
   int64_t total = 0;
   for (int h = 0; h < prob->heads; ++h) {
     const int k = topk_count(sel->head_param_bp[h], (int)nb, n_text);
@@ -234,9 +261,15 @@ adaspa_status adaspa_block_search(const adaspa_problem* prob, const void* q, con
   P.kmin = n_text > 1 ? n_text : 1;
   P.mode = sel->mode;
   P.cap = (int64_t)((((uint64_t)1) << 62) / ((uint64_t)nb * (uint64_t)nb));
-  for (int h = 0; h < prob->heads; ++h)
-    P.head_param[h] = sel->mode == ADASPA_SELECT_TOPK ? topk_count(sel->head_param_bp[h], nb, n_text)
-                                                      : sel->head_param_bp[h];
+  if (sel->mode == ADASPA_SELECT_HIERARCHICAL) {
+    hierarchical_counts(sel->base_sparsity_bp, nb, n_text, &P.k_base, &P.k_hi, &P.k_lo);
+    P.recall_thr_bp = sel->recall_threshold_bp;
+  } else {
+    for (int h = 0; h < prob->heads; ++h)
+      P.head_param[h] = sel->mode == ADASPA_SELECT_TOPK
+                            ? topk_count(sel->head_param_bp[h], nb, n_text)
+                            : sel->head_param_bp[h];
+  }
   return launch_select(P, s) == hipSuccess ? ADASPA_OK : ADASPA_ERR_HIP;
 }
 

@@ -62,7 +62,9 @@ struct SelectParams {
   int nb;
   int text_lo, text_hi;       // text block range [lo, hi]; lo > hi when none
   int kmin;                   // smallest allowed count, max(1, #text blocks)
-  int mode;                   // 0 = TOPK, 1 = COVERAGE
+  int mode;                   // 0 = TOPK, 1 = COVERAGE, 2 = HIERARCHICAL
+  int k_base, k_hi, k_lo;     // HIERARCHICAL: counts at s, (1+s)/2 and (3s-1)/2
+  int recall_thr_bp;          // HIERARCHICAL: Recall threshold
   int64_t cap;                // Q32 cap = floor(2^62 / (nb*nb))
   int32_t head_param[kMaxHeads];  // TOPK: k_h; COVERAGE: tau_bp
 };

@@ -154,6 +154,24 @@ __global__ __launch_bounds__(SEL_NT) void select_heads_kernel(SelectParams P) {
       int k;
       if (P.mode == 0) {
         k = P.head_param[hh];
+      } else if (P.mode == 2) {
+        // Recall of every head of this batch element at the base count; a
+        // head with no mass has Recall 1.  Ranks compare kept/total exactly.
+        const int b = bh / P.heads;
+        const int kb = P.k_base;
+        uint64_t ka = (uint64_t)cv[kb - 1], ta = (uint64_t)total;
+        if (ta == 0) { ka = 1; ta = 1; }
+        int n_above = 0, rank = 0;
+        for (int h2 = 0; h2 < P.heads; ++h2) {
+          const int64_t* c2 = P.ws_curve + (size_t)(b * P.heads + h2) * nb;
+          uint64_t k2 = (uint64_t)c2[kb - 1], t2 = (uint64_t)c2[nb - 1];
+          if (t2 == 0) { k2 = 1; t2 = 1; }
+          n_above += ((unsigned __int128)k2 * 10000u > (unsigned __int128)t2 * (uint64_t)P.recall_thr_bp);
+          const unsigned __int128 lhs = (unsigned __int128)k2 * ta, rhs = (unsigned __int128)ka * t2;
+          rank += (lhs > rhs) || (lhs == rhs && h2 < hh);
+        }
+        const int n = n_above < P.heads / 2 ? n_above : P.heads / 2;
+        k = rank < n ? P.k_hi : (rank >= P.heads - n ? P.k_lo : kb);
       } else {
         const unsigned __int128 need = (unsigned __int128)(uint64_t)total * (uint64_t)P.head_param[hh];
         int lo = P.kmin, hi = nb;   // smallest k in [lo, hi] with kept(k)*10000 >= need

@@ -96,6 +96,20 @@ def test_capacity_and_workspace(lib):
     assert lib.adaspa_block_search_capacity(ctypes.byref(p), ctypes.byref(bad2)) == -1
 
 
+def test_hierarchical_capacity_and_validation(lib):
+    import oracle
+    p = _prob(seqlen=110336, heads=3, head_dim=128, block=128, text_len=256)
+    for base in (0, 5000, 8000, 9000, 10000):
+        s = ad._Select(2, 1, None, base, 8000)
+        s_hi, s_lo = (10000 + base) // 2, max(0, (3 * base - 10000) // 2)
+        kmax = max(oracle.topk_count(10000 - x, 862, 2) for x in (base, s_hi, s_lo))
+        assert lib.adaspa_block_search_capacity(ctypes.byref(p), ctypes.byref(s)) == 3 * (2 * 862 + 860 * kmax)
+        assert lib.adaspa_block_search_workspace(ctypes.byref(p), ctypes.byref(s)) > 0
+    for bad in ((-1, 8000), (10001, 8000), (8000, -1), (8000, 10001)):
+        s = ad._Select(2, 1, None, *bad)
+        assert lib.adaspa_block_search_capacity(ctypes.byref(p), ctypes.byref(s)) == -1
+
+
 def test_capacity_matches_oracle_counts(lib):
     import oracle
     for keep in (0, 1, 500, 1000, 2000, 5000, 10000):

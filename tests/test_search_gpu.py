@@ -192,3 +192,25 @@ def test_search_end_to_end_against_oracle(w, heads):
             kth = _kth_mass(np.array([Wref[0, h, p, c] for c in range(nb) if c not in tk]), kh - len(tk))
             for c in got ^ exp:
                 assert abs(Wref[0, h, p, c] - kth) <= 1e-3 * kth, (h, p, c)
+
+
+@pytest.mark.parametrize("case", CASES)
+@pytest.mark.parametrize("base_bp,thr_bp", [(8000, 8000), (9000, 5000), (5000, 9000), (3000, 0)])
+def test_hierarchical_selection_bit_exact(case, base_bp, thr_bp):
+    """Head-adaptive hierarchical mode (Sec. 4.2): counts, ranks and indices
+    bit-exact against the oracle on identical scores, with heads whose mass is
+    concentrated to different degrees (so some heads move up and some down)."""
+    B, H, L, block, ts, tl = case
+    nb = (L + block - 1) // block
+    W = random_block_masses((B, H, nb, nb), seed=H + nb + base_bp)
+    # head h: diagonal-heavy by a factor that falls with h, so Recall varies
+    boost = torch.tensor([8.0 / (1 + h) ** 2 for h in range(H)]).view(1, H, 1, 1)
+    W = W + boost * torch.eye(nb).view(1, 1, nb, nb) * W.mean()
+    W = W.to(torch.float32)
+    res = ad.block_search(None, None, None, block=block, text_start=ts, text_len=tl,
+                          mode="hierarchical", base_sparsity_bp=base_bp, recall_threshold_bp=thr_bp,
+                          scores=W.cuda(), shape=(B, H, L, 64))
+    torch.cuda.synchronize()
+    sel = oracle.select_blocks(W.numpy(), L, block, ts, tl, "hierarchical", [0] * H,
+                               base_sparsity_bp=base_bp, recall_threshold_bp=thr_bp)
+    _compare_selection(res, sel)
