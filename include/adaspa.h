@@ -50,7 +50,8 @@ extern "C" {
 typedef enum {
   ADASPA_OK = 0,
   ADASPA_ERR_INVALID_ARG = 1,   /* null/misaligned pointer, bad size or range */
-  ADASPA_ERR_UNSUPPORTED = 2,   /* head_dim or block outside what is built    */
+  ADASPA_ERR_UNSUPPORTED = 2,   /* head_dim or block outside what is built,
+                                   L * D >= 2^30, or B * H >= 65536            */
   ADASPA_ERR_CAPACITY = 3,      /* col_idx capacity too small                 */
   ADASPA_ERR_WORKSPACE = 4,     /* workspace missing or too small             */
   ADASPA_ERR_HIP = 5            /* a HIP launch reported an error             */
@@ -59,7 +60,8 @@ typedef enum {
 /* Shape of one attention call: B batches x H heads of L tokens with head
  * dimension D; square sparse blocks of Bs tokens.  Supported: D in {64, 128},
  * Bs in {64, 128}, L >= 1 (L need not be a multiple of Bs: the last block is
- * ragged and out-of-range keys never contribute).  softmax_scale <= 0 selects
+ * ragged and out-of-range keys never contribute), L * D < 2^30 and B * H <
+ * 65536 (larger shapes return ADASPA_ERR_UNSUPPORTED).  softmax_scale <= 0 selects
  * 1/sqrt(D) (the attention-weights equation, Sec. 2.2). */
 typedef struct {
   int32_t batch, heads, seqlen, head_dim;

@@ -31,8 +31,8 @@ adaspa_status check_problem(const adaspa_problem* p) {
   if (!(isfinite(p->softmax_scale))) return ADASPA_ERR_INVALID_ARG;
   if (p->head_dim != 64 && p->head_dim != 128) return ADASPA_ERR_UNSUPPORTED;
   if (p->block != 64 && p->block != 128) return ADASPA_ERR_UNSUPPORTED;
-  // Per-head element offsets are 32-bit inside the kernels.
-  if ((int64_t)p->seqlen * p->head_dim >= ((int64_t)1 << 31)) return ADASPA_ERR_UNSUPPORTED;
+  // Per-head byte offsets inside the kernels stay below 2^31.
+  if ((int64_t)p->seqlen * p->head_dim >= ((int64_t)1 << 30)) return ADASPA_ERR_UNSUPPORTED;
   if ((int64_t)p->batch * p->heads >= 65536) return ADASPA_ERR_UNSUPPORTED;
   return ADASPA_OK;
 }

@@ -24,7 +24,7 @@ namespace adaspa {
 // same.
 // ---------------------------------------------------------------------------
 template <int D, int NW, bool SPARSE>
-__global__ __launch_bounds__(64 * NW, 2) void attn_fwd_kernel(AttnParams a) {
+__global__ __launch_bounds__(64 * NW, NW >= 8 ? 1 : 2) void attn_fwd_kernel(AttnParams a) {
   constexpr int NT = 64 * NW;
   using KDMA = TileDMA<D, NW, 1>;
   using VDMA = TileDMA<D, NW, 2>;
@@ -124,8 +124,12 @@ __global__ __launch_bounds__(64 * NW, 2) void attn_fwd_kernel(AttnParams a) {
     bool pend = false;
     float pend_alpha = 1.f;
 
+    KVLoader<D, NW> ld;
+    ld.init(wave, lane);
+
     // Step t reads K(t+1) and V(t-1) from buffer (t+1)&1 and loads K(t+2),
-    // V(t) into buffer t&1.
+    // V(t) into buffer t&1.  The loads are spread over the MFMA slots of the
+    // step: this wave's K instructions first, then its V instructions.
     auto step = [&](int t, const u16* rdK, const u16* rdV, u16* ldK, u16* ldV) {
       if (pend) {
 #pragma unroll
@@ -133,12 +137,26 @@ __global__ __launch_bounds__(64 * NW, 2) void attn_fwd_kernel(AttnParams a) {
 #pragma unroll
           for (int e = 0; e < 16; ++e) o[d][e] *= pend_alpha;
       }
-      if (t + 2 < nf) KDMA::issue(rK, ldK, kbase(t + 2), wave, lane);
-      VDMA::issue(rV, ldV, kbase(t), wave, lane);
+      const bool kload = t + 2 < nf;
+      const uint32_t kbyte = kload ? (uint32_t)kbase(t + 2) * (uint32_t)(D * 2) : 0u;
+      const uint32_t vbyte = (uint32_t)kbase(t) * (uint32_t)(D * 2);
+      auto loads = [&](int slot) {
+        // Instruction n goes to slot n * NM / NTOT (at most one per slot).
+        constexpr int PK = KVLoader<D, NW>::PWK, NTOT = PK + KVLoader<D, NW>::PWV;
+        constexpr int NM = 2 * NK + 4 * ND;
+        static_assert(NTOT <= NM, "one load instruction per slot at most");
+        const int n = (slot * NTOT + NM - 1) / NM;
+        if (n >= NTOT || (n * NM) / NTOT != slot) return;
+        if (n < PK) {
+          if (kload) ld.k(rK, ldK, kbyte, n, wave);
+        } else {
+          ld.v(rV, ldV, vbyte, n - PK, wave);
+        }
+      };
       f32x16 s_next[2];
       bf16x8 p_cur[2][2];
-      pipelined_step<D, KS, VS>(rdK + klane, rdV + voff, qf, s_cur, p_prev, s_next, p_cur, o, m, lsum,
-                                thr, sl2, pend_alpha, pend);
+      pipelined_step<D, KS, VS>(loads, rdK + klane, rdV + voff, qf, s_cur, p_prev, s_next, p_cur, o, m,
+                                lsum, thr, sl2, pend_alpha, pend);
 #pragma unroll
       for (int g = 0; g < 2; ++g) {
         s_cur[g] = s_next[g];
@@ -148,10 +166,12 @@ __global__ __launch_bounds__(64 * NW, 2) void attn_fwd_kernel(AttnParams a) {
       wait_vmem();
       __syncthreads();
     };
-    for (int t = 0; t < nf; t += 2) {
+    int t = 0;
+    for (; t + 1 < nf; t += 2) {
       step(t, sK1, sV1, sK0, sV0);
-      if (t + 1 < nf) step(t + 1, sK0, sV0, sK1, sV1);
+      step(t + 1, sK0, sV0, sK1, sV1);
     }
+    if (t < nf) step(t, sK1, sV1, sK0, sV0);
     if (pend) {
 #pragma unroll
       for (int d = 0; d < ND; ++d)
@@ -326,13 +346,14 @@ static hipError_t launch_attn(const AttnParams& a, hipStream_t st) {
 }
 
 hipError_t launch_dense(AttnParams a, int D, hipStream_t st) {
-  // 128 query rows per workgroup (four waves of 32 rows).
+  // 256 query rows per workgroup (eight waves of 32 rows): every K/V tile
+  // brought into LDS serves twice the rows of a 128-row workgroup.
   a.row_ptr = nullptr;
   a.col_idx = nullptr;
-  a.nqt = (a.seqlen + 127) / 128;
+  a.nqt = (a.seqlen + 255) / 256;
   a.n_wg = a.nqt * a.batch_heads;
-  if (D == 64) return launch_attn<64, 4, false>(a, st);
-  return launch_attn<128, 4, false>(a, st);
+  if (D == 64) return launch_attn<64, 8, false>(a, st);
+  return launch_attn<128, 8, false>(a, st);
 }
 
 hipError_t launch_sparse(AttnParams a, int D, hipStream_t st) {

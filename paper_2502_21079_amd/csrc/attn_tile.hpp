@@ -66,12 +66,71 @@ struct TileDMA {
       }
     }
   }
+
+  // Byte offset, inside the tile, of the chunk that slot i * 64 + lane loads
+  // when every row of the tile lies inside the sequence.  A pad slot loads a
+  // copy of its row's last data chunk (it is never read, and an in-range
+  // duplicate keeps every offset below 2^16).
+  __device__ __forceinline__ static uint32_t rel_offset(int i, int lane) {
+    const int p = i * 64 + lane;
+    const int row = p / S, ch = p % S;
+    return (uint32_t)(row * D + (ch < CPR ? ch : CPR - 1) * 8) * 2u;
+  }
+  // Instruction i of a full tile whose first byte is tile_byte: the offset
+  // inside the tile comes from rel_offset, the tile start is the scalar
+  // offset, so an issue costs no address arithmetic.
+  __device__ __forceinline__ static void issue_full(__amdgpu_buffer_rsrc_t r, u16* dst,
+                                                    uint32_t tile_byte, int i, uint32_t rel) {
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (lds_void*)(dst + i * 64 * 8), 16, rel,
+                                             (int)tile_byte, 0, 0);
+  }
 };
 using std::integral_constant;
+
+// Loads of one full K tile and one full V tile spread over a step.  Wave w
+// owns instructions i = j * NW + w of each tile; the two 16-bit in-tile
+// offsets of instruction j are kept packed in one register (K low, V high).
+template <int D, int NW>
+struct KVLoader {
+  using K = TileDMA<D, NW, 1>;
+  using V = TileDMA<D, NW, 2>;
+  static constexpr int PWK = (K::NINST + NW - 1) / NW;
+  static constexpr int PWV = (V::NINST + NW - 1) / NW;
+  static constexpr int PW = PWK > PWV ? PWK : PWV;
+  static_assert(KT * D * 2 <= 65536, "in-tile offsets must fit in 16 bits");
+  uint32_t rel[PW];
+
+  __device__ __forceinline__ void init(int wave, int lane) {
+#pragma unroll
+    for (int j = 0; j < PW; ++j) {
+      const int i = j * NW + wave;
+      const uint32_t k = i < K::NINST ? K::rel_offset(i, lane) : 0u;
+      const uint32_t v = i < V::NINST ? V::rel_offset(i, lane) : 0u;
+      rel[j] = k | (v << 16);
+    }
+  }
+  __device__ __forceinline__ void k(__amdgpu_buffer_rsrc_t r, u16* dst, uint32_t tile_byte, int j,
+                                    int wave) const {
+    const int i = j * NW + wave;
+    if (j < PWK && i < K::NINST) K::issue_full(r, dst, tile_byte, i, rel[j] & 0xFFFFu);
+  }
+  __device__ __forceinline__ void v(__amdgpu_buffer_rsrc_t r, u16* dst, uint32_t tile_byte, int j,
+                                    int wave) const {
+    const int i = j * NW + wave;
+    if (j < PWV && i < V::NINST) V::issue_full(r, dst, tile_byte, i, rel[j] >> 16);
+  }
+};
+
 
 // Maximum without the sNaN canonicalisation that fmaxf needs in IEEE mode
 // (a NaN score propagates, which is fine: the row is then NaN either way).
 __device__ __forceinline__ float vmax(float a, float b) { return __builtin_elementwise_maximum(a, b); }
+
+// Keeps the computation of v at this point of the instruction stream: the
+// empty volatile asm is ordered with the scheduling fences around it, so the
+// compiler can neither sink the work that produces v past them (out of the
+// MFMA slot it was placed in) nor hoist it.
+__device__ __forceinline__ void pin(float& v) { asm volatile("" : "+v"(v)); }
 
 __device__ __forceinline__ void wait_vmem() { __builtin_amdgcn_s_waitcnt(0x0F70); }   // vmcnt(0)
 
@@ -180,11 +239,13 @@ __device__ __forceinline__ void pv_tile(const u16* vlane, const bf16x8 (&pb)[2][
 // One pipelined step, scheduled by hand: NM = 2*NK + 4*ND MFMA slots that
 // alternate a QK MFMA (scores of the next tile) and a PV MFMA (output update
 // of the previous tile).  Each slot first issues the LDS operand reads of the
-// slot LA places ahead, then its MFMA, then a fixed slice of the softmax of
-// the current tile; a scheduling fence closes the slot, so the matrix pipe
-// and the VALU work side by side within the wave.
-template <int D, int KS, int VS>
-__device__ __forceinline__ void pipelined_step(const u16* klane, const u16* vlane,
+// slot LA places ahead, then its MFMA, then hook(slot) (the caller's tile
+// loads, spread over the step so the load path never stalls the wave for
+// long), then a fixed slice of the softmax of the current tile; a scheduling
+// fence closes the slot, so the matrix pipe and the VALU work side by side
+// within the wave.
+template <int D, int KS, int VS, typename Hook>
+__device__ __forceinline__ void pipelined_step(Hook&& hook, const u16* klane, const u16* vlane,
                                                const bf16x8 (&qf)[D / 16], const f32x16 (&s_cur)[2],
                                                const bf16x8 (&p_prev)[2][2], f32x16 (&s_next)[2],
                                                bf16x8 (&p_cur)[2][2], f32x16 (&o)[D / 32], float& m,
@@ -239,6 +300,7 @@ __device__ __forceinline__ void pipelined_step(const u16* klane, const u16* vlan
         const int g = q >> 3, e = (q & 7) * 2;
         mt = vmax(mt, vmax(s_cur[g][e], s_cur[g][e + 1]));
       }
+      pin(mt);
     } else if (i == SHFL) {
       mtx = __shfl_xor(mt, 32, 64);
     } else if (i == MC) {
@@ -249,6 +311,7 @@ __device__ __forceinline__ void pipelined_step(const u16* klane, const u16* vlan
       lsum *= alpha;
       m = mnew;
       mc = (m == -INFINITY) ? 0.f : m * sl2;
+      pin(mc);
     } else if (i >= P2) {
       // 32 exponentials in groups of 4 (one bf16x4 quarter of p_cur)
       constexpr int NQ = 8;                   // quarters of 4 elements
@@ -266,6 +329,7 @@ __device__ __forceinline__ void pipelined_step(const u16* klane, const u16* vlan
           lsum = __builtin_amdgcn_fdot2_f32_bf16(pr, ones, lsum, false);
         }
       }
+      pin(lsum);
     }
   };
 
@@ -275,6 +339,7 @@ __device__ __forceinline__ void pipelined_step(const u16* klane, const u16* vlan
   for (int i = 0; i < NM; ++i) {
     if (i + LA < NM) fetch(i + LA);
     mfma(i);
+    hook(i);
     valu(i);
     __builtin_amdgcn_sched_barrier(0);
   }
