@@ -31,7 +31,8 @@ adaspa_status check_problem(const adaspa_problem* p) {
   if (!(isfinite(p->softmax_scale))) return ADASPA_ERR_INVALID_ARG;
   if (p->head_dim != 64 && p->head_dim != 128) return ADASPA_ERR_UNSUPPORTED;
   if (p->block != 64 && p->block != 128) return ADASPA_ERR_UNSUPPORTED;
-  // Per-head byte offsets inside the kernels stay below 2^31.
+  // Per-head byte sizes stay below 2^31, so every in-kernel byte offset (the
+  // out-of-range offset of a skipped slot included) fits in 32 bits.
   if ((int64_t)p->seqlen * p->head_dim >= ((int64_t)1 << 30)) return ADASPA_ERR_UNSUPPORTED;
   if ((int64_t)p->batch * p->heads >= 65536) return ADASPA_ERR_UNSUPPORTED;
   return ADASPA_OK;

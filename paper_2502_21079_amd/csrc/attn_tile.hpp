@@ -238,7 +238,10 @@ __device__ __forceinline__ void pv_tile(const u16* vlane, const bf16x8 (&pb)[2][
 
 // One pipelined step, scheduled by hand: NM = 2*NK + 4*ND MFMA slots that
 // alternate a QK MFMA (scores of the next tile) and a PV MFMA (output update
-// of the previous tile).  Each slot first issues the LDS operand reads of the
+// of the previous tile).  The QK MFMAs alternate between the two 32-key score
+// groups and the PV MFMAs rotate over the ND output blocks, so two MFMAs into
+// the same accumulator are 4 (QK) or 2*ND (PV) slots apart and one wave alone
+// keeps the matrix pipe busy; each accumulator still sums in the same order.  Each slot first issues the LDS operand reads of the
 // slot LA places ahead, then its MFMA, then hook(slot) (the caller's tile
 // loads, spread over the step so the load path never stalls the wave for
 // long), then a fixed slice of the softmax of the current tile; a scheduling
@@ -264,11 +267,11 @@ __device__ __forceinline__ void pipelined_step(Hook&& hook, const u16* klane, co
   bf16x8 op[NM];
   auto fetch = [&](int i) {
     const int j = i >> 1;
-    if ((i & 1) == 0) {       // QK j: g = j / NK, ks = j % NK
-      const int g = j / NK, ks = j % NK;
+    if ((i & 1) == 0) {       // QK j: g = j % 2, ks = j / 2
+      const int g = j & 1, ks = j >> 1;
       op[i] = *reinterpret_cast<const bf16x8*>(klane + (32 * g * KS + 2 * ks) * 8);
-    } else {                  // PV j: d = j / 4, g = (j / 2) % 2, s2 = j % 2
-      const int d = j >> 2, g = (j >> 1) & 1, s2 = j & 1;
+    } else {                  // PV j: d = j % ND, (g, s2) = j / ND
+      const int d = j % ND, g = (j / ND) >> 1, s2 = (j / ND) & 1;
       const u16* p0 = vlane + (32 * g + 16 * s2) * VS * 8 + d * 32;
       const s16x4 lo = lds_read_tr16(p0);
       const s16x4 hi = lds_read_tr16(p0 + 8 * VS * 8);
@@ -279,11 +282,11 @@ __device__ __forceinline__ void pipelined_step(Hook&& hook, const u16* klane, co
   auto mfma = [&](int i) {
     const int j = i >> 1;
     if ((i & 1) == 0) {
-      const int g = j / NK, ks = j % NK;
+      const int g = j & 1, ks = j >> 1;
       if (ks == 0) s_next[g] = mfma32(op[i], qf[ks], f32x16{});
       else s_next[g] = mfma32(op[i], qf[ks], s_next[g]);
     } else {
-      const int d = j >> 2, g = (j >> 1) & 1, s2 = j & 1;
+      const int d = j % ND, g = (j / ND) >> 1, s2 = (j / ND) & 1;
       o[d] = mfma32(op[i], p_prev[g][s2], o[d]);
     }
   };
