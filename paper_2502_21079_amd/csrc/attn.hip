@@ -239,16 +239,25 @@ __global__ __launch_bounds__(64 * NW, NW >= 8 ? 1 : 2) void attn_fwd_kernel(Attn
 
 // ---------------------------------------------------------------------------
 // Block attention mass: W[p][c] = sum_{i in p, j in c} exp(scale*q_i.k_j - LSE_i)
+//
+// One workgroup per query block p (32 rows per wave).  Full key tiles run
+// through a software pipeline: step t forms the scores of tile t+1 (QK MFMAs)
+// while the VALU exponentiates and sums tile t; K is double-buffered and the
+// loads of tile t+2 are spread over the step.  Per-wave sums of a finished
+// key block are combined in a fixed order into an LDS ring of row p, which
+// is written out 64 blocks at a time (coalesced).
 // ---------------------------------------------------------------------------
 template <int D, int NW>
-__global__ __launch_bounds__(64 * NW, 2) void block_mass_kernel(MassParams a) {
+__global__ __launch_bounds__(64 * NW, 8 / NW) void block_mass_kernel(MassParams a) {
   constexpr int NT = 64 * NW;
   using KDMA = TileDMA<D, NW, 1>;
   constexpr int KS = KDMA::S;
   constexpr int NK = D / 16;
   __shared__ __attribute__((aligned(1024))) u16 sK0[KDMA::ELEMS];
   __shared__ __attribute__((aligned(1024))) u16 sK1[KDMA::ELEMS];
+  constexpr int RING = 128, CHUNK = 64;
   __shared__ float sRed[2][NW];     // per-wave sums of the last two blocks
+  __shared__ float sW[RING];        // blocks of row p not yet written out
 
   int bh, p;
   if (a.xcd_map == 2) {
@@ -271,69 +280,113 @@ __global__ __launch_bounds__(64 * NW, 2) void block_mass_kernel(MassParams a) {
   zero_lds<KDMA::SLOTS>(sK1, tid, NT);
   bf16x8 qf[NK];
   load_q<D>(a.q + hoff, qrow, L, hw, qf);
-  const float lse2 = qvalid ? a.lse[(size_t)bh * L + qrow] * kLog2e : INFINITY;
   const float sl2 = a.scale_log2;
+  // A padding row (past L) gets -inf: exp2 of it is 0 and it adds nothing.
+  const float nlse2 = qvalid ? -a.lse[(size_t)bh * L + qrow] * kLog2e : -INFINITY;
   const int sub = a.block / KT;
-  const int ntile = a.nkb * sub;
+  const int nfull = L / KT;   // full key tiles
   float* wrow = a.w + ((size_t)bh * a.nkb + p) * a.nkb;
 
-  __syncthreads();
-  if (L >= KT) KDMA::issue(rK, sK0, 0, wave, lane);
-  wait_vmem();
-  __syncthreads();
-
   float acc = 0.f;
-  auto tile = [&](auto masked, const u16* cK, int kb) {
-    f32x16 s[2];
-    qk_tile<D, KS>(cK, qf, c32, hw, s);
-    if constexpr (decltype(masked)::value) mask_tile(s, L - kb, hw);
-#pragma unroll
-    for (int g = 0; g < 2; ++g)
-#pragma unroll
-      for (int e = 0; e < 16; ++e) acc += fast_exp2(fmaf(s[g][e], sl2, -lse2));
-  };
-  // Full tiles in the loop; a block whose last tile is ragged (or missing)
-  // is finished after it, with the masked tile.
-  const int nfull = L / KT;
   auto finish_block = [&](int blk) {
     const float w = wave_sum(acc);
     if (lane == 0) sRed[blk & 1][wave] = w;
     acc = 0.f;
   };
+  // After a barrier: waves combined in a fixed order (deterministic).
   auto publish = [&](int blk) {
-    // Waves are combined in a fixed order, so the result is deterministic.
     if (tid == 0) {
       float v = 0.f;
 #pragma unroll
       for (int w = 0; w < NW; ++w) v += sRed[blk & 1][w];
-      wrow[blk] = v;
+      sW[blk % RING] = v;
     }
   };
-  auto step = [&](int t, const u16* cK, u16* nK) {
-    const int kb = t * KT;
-    if (t + 1 < nfull) KDMA::issue(rK, nK, kb + KT, wave, lane);
-    tile(std::false_type{}, cK, kb);
-    const bool block_end = (t + 1) % sub == 0;
-    if (block_end) finish_block(t / sub);
+  // After a barrier that follows the publication of block blk: once a chunk
+  // of CHUNK blocks is complete, write it out (it is not touched again until
+  // the ring wraps, CHUNK blocks and at least one barrier later).
+  int flushed = 0;                  // blocks [0, flushed) written out
+  auto flush = [&](int done) {      // blocks [0, done) published
+    while (done - flushed >= CHUNK) {
+      if (tid < CHUNK) wrow[flushed + tid] = sW[(flushed + tid) % RING];
+      flushed += CHUNK;
+    }
+  };
+  __syncthreads();
+
+  if (nfull > 0) {
+    KDMA::issue(rK, sK0, 0, wave, lane);
+    if (nfull > 1) KDMA::issue(rK, sK1, KT, wave, lane);
     wait_vmem();
     __syncthreads();
-    if (block_end) publish(t / sub);
-  };
-  for (int t = 0; t < nfull; t += 2) {
-    step(t, sK0, sK1);
-    if (t + 1 < nfull) step(t + 1, sK1, sK0);
+    f32x16 s_cur[2];
+    qk_tile<D, KS>(sK0, qf, c32, hw, s_cur);
+    __syncthreads();            // sK0 is refilled by step 0
+
+    KLoader<D, NW> ld;
+    ld.init(wave, lane);
+    const int klane = (c32 * KS + hw) * 8;
+    // Step t (t + 1 < nfull) sums tile t, forms the scores of tile t+1 from
+    // buffer (t+1)&1 and loads tile t+2 into buffer t&1.
+    auto step = [&](int t, const u16* rdK, u16* ldK) {
+      const bool kload = t + 2 < nfull;
+      const uint32_t kbyte = (uint32_t)(t + 2) * (uint32_t)(KT * D * 2);
+      auto loads = [&](int slot) {
+        constexpr int NTOT = KLoader<D, NW>::PW, NM = 2 * NK;
+        static_assert(NTOT <= NM, "one load instruction per slot at most");
+        const int n = (slot * NTOT + NM - 1) / NM;
+        if (n >= NTOT || (n * NM) / NTOT != slot) return;
+        if (kload) ld.k(rK, ldK, kbyte, n, wave);
+      };
+      f32x16 s_next[2];
+      mass_step<D, KS>(loads, rdK + klane, qf, s_cur, s_next, acc, sl2, nlse2);
+      s_cur[0] = s_next[0];
+      s_cur[1] = s_next[1];
+      const bool block_end = (t + 1) % sub == 0;
+      if (block_end) finish_block(t / sub);
+      wait_vmem();
+      __syncthreads();
+      flush(t / sub);               // blocks published before this barrier
+      if (block_end) publish(t / sub);
+    };
+    int t = 0;
+    for (; t + 2 < nfull; t += 2) {
+      step(t, sK1, sK0);
+      step(t + 1, sK0, sK1);
+    }
+    if (t + 1 < nfull) {
+      step(t, sK1, sK0);
+      ++t;
+    }
+    // Last full tile: its scores are in s_cur.
+#pragma unroll
+    for (int e = 0; e < 32; ++e) acc += fast_exp2(fmaf(s_cur[e >> 4][e & 15], sl2, nlse2));
+    if ((t + 1) % sub == 0) {
+      finish_block(t / sub);
+      __syncthreads();
+      publish(t / sub);
+    }
   }
-  if (nfull < ntile && nfull * KT < L) {
+  // Ragged last tile (L not a multiple of KT), with key masking.
+  if (nfull * KT < L) {
+    __syncthreads();
     KDMA::issue(rK, sK0, nfull * KT, wave, lane);
     wait_vmem();
     __syncthreads();
-    tile(std::true_type{}, sK0, nfull * KT);
+    f32x16 s[2];
+    qk_tile<D, KS>(sK0, qf, c32, hw, s);
+    mask_tile(s, L - nfull * KT, hw);
+#pragma unroll
+    for (int e = 0; e < 32; ++e) acc += fast_exp2(fmaf(s[e >> 4][e & 15], sl2, nlse2));
   }
+  // The last block, when its tiles did not end on a block boundary.
   if (nfull % sub != 0 || nfull * KT < L) {
     finish_block(a.nkb - 1);
     __syncthreads();
     publish(a.nkb - 1);
   }
+  __syncthreads();
+  for (int i = flushed + tid; i < a.nkb; i += NT) wrow[i] = sW[i % RING];
 }
 
 // ---------------------------------------------------------------------------

@@ -87,6 +87,28 @@ struct TileDMA {
 };
 using std::integral_constant;
 
+// Loads of one full K tile spread over a step (the block-mass pass).
+template <int D, int NW>
+struct KLoader {
+  using K = TileDMA<D, NW, 1>;
+  static constexpr int PW = (K::NINST + NW - 1) / NW;
+  uint32_t rel[PW];
+
+  __device__ __forceinline__ void init(int wave, int lane) {
+#pragma unroll
+    for (int j = 0; j < PW; ++j) {
+      const int i = j * NW + wave;
+      rel[j] = i < K::NINST ? K::rel_offset(i, lane) : 0u;
+    }
+  }
+  __device__ __forceinline__ void k(__amdgpu_buffer_rsrc_t r, u16* dst, uint32_t tile_byte, int j,
+                                    int wave) const {
+    const int i = j * NW + wave;
+    if (i < K::NINST) K::issue_full(r, dst, tile_byte, i, rel[j]);
+  }
+};
+
+
 // Loads of one full K tile and one full V tile spread over a step.  Wave w
 // owns instructions i = j * NW + w of each tile; the two 16-bit in-tile
 // offsets of instruction j are kept packed in one register (K low, V high).
@@ -336,6 +358,43 @@ __device__ __forceinline__ void pipelined_step(Hook&& hook, const u16* klane, co
     }
   };
 
+#pragma unroll
+  for (int i = 0; i < LA; ++i) fetch(i);
+#pragma unroll
+  for (int i = 0; i < NM; ++i) {
+    if (i + LA < NM) fetch(i + LA);
+    mfma(i);
+    hook(i);
+    valu(i);
+    __builtin_amdgcn_sched_barrier(0);
+  }
+}
+
+// One pipelined step of the block-mass pass: the NM = 2*NK QK MFMAs of the
+// next tile (alternating the two 32-key groups) with, slot by slot, an equal
+// share of the exp2(s * sl2 - lse2) terms of the current tile added to acc in
+// (group, element) order; hook(slot) issues the caller's tile loads.
+template <int D, int KS, typename Hook>
+__device__ __forceinline__ void mass_step(Hook&& hook, const u16* klane, const bf16x8 (&qf)[D / 16],
+                                          const f32x16 (&s_cur)[2], f32x16 (&s_next)[2], float& acc,
+                                          float sl2, float nlse2) {
+  constexpr int NK = D / 16, NM = 2 * NK, LA = 2;
+  bf16x8 op[NM];
+  auto fetch = [&](int j) {
+    const int g = j & 1, ks = j >> 1;
+    op[j] = *reinterpret_cast<const bf16x8*>(klane + (32 * g * KS + 2 * ks) * 8);
+  };
+  auto mfma = [&](int j) {
+    const int g = j & 1, ks = j >> 1;
+    if (ks == 0) s_next[g] = mfma32(op[j], qf[ks], f32x16{});
+    else s_next[g] = mfma32(op[j], qf[ks], s_next[g]);
+  };
+  auto valu = [&](int j) {
+    const int e0 = j * 32 / NM, e1 = (j + 1) * 32 / NM;
+#pragma unroll
+    for (int e = e0; e < e1; ++e) acc += fast_exp2(fmaf(s_cur[e >> 4][e & 15], sl2, nlse2));
+    pin(acc);
+  };
 #pragma unroll
   for (int i = 0; i < LA; ++i) fetch(i);
 #pragma unroll

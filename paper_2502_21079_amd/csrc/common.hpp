@@ -68,10 +68,24 @@ __device__ __forceinline__ void xcd_chunk_map(int bid, int nqt, int nbh, int& bh
   qt = c0 + rel % sz;
 }
 
+// Sum over the 64 lanes of a wave, returned to every lane.  DPP moves sum
+// within each row of 16 lanes (no LDS round trips); the four row sums are
+// then read out and added in a fixed order, so the result is deterministic.
+template <int CTRL>
+__device__ __forceinline__ float dpp_plus(float v) {
+  const int moved = __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, v), CTRL, 0xF, 0xF, false);
+  return v + __builtin_bit_cast(float, moved);
+}
 __device__ __forceinline__ float wave_sum(float v) {
-#pragma unroll
-  for (int o = 32; o >= 1; o >>= 1) v += __shfl_xor(v, o, 64);
-  return v;
+  v = dpp_plus<0xB1>(v);    // quad_perm [1,0,3,2]: pairs
+  v = dpp_plus<0x4E>(v);    // quad_perm [2,3,0,1]: quads
+  v = dpp_plus<0x124>(v);   // row_ror:4: two quads
+  v = dpp_plus<0x128>(v);   // row_ror:8: whole row of 16
+  const float r0 = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, v), 0));
+  const float r1 = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, v), 16));
+  const float r2 = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, v), 32));
+  const float r3 = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, v), 48));
+  return (r0 + r1) + (r2 + r3);
 }
 
 }  // namespace adaspa
