@@ -119,9 +119,9 @@ namespace adaspa {
 // Work-to-XCD mapping (see the kernels): 1 gives each XCD one contiguous range
 // of (head, query tile) work items, so the workgroups sharing an L2 stream the
 // same K/V (dense attention and the mass pass: about 6x less HBM traffic than
-// hardware order); 0 keeps the hardware's round-robin order, which balances
-// heads of different cost (block-sparse attention with per-head densities);
-// 2 is the head-chunked order.  ADASPA_XCD_MAP overrides the per-kernel choice.
+// hardware order; block-sparse attention: neighbouring query blocks select
+// largely the same key blocks); 0 keeps the hardware's round-robin order; 2 is
+// the head-chunked order.  ADASPA_XCD_MAP overrides the per-kernel choice.
 int xcd_map_mode(int kernel_default) {
   static const int env = [] {
     const char* e = getenv("ADASPA_XCD_MAP");
@@ -302,7 +302,7 @@ adaspa_status adaspa_block_sparse_attn(const adaspa_problem* prob, const void* q
   a.nkb = num_blocks(prob);
   a.scale = scale_of(prob);
   a.scale_log2 = a.scale * 1.4426950408889634f;
-  a.xcd_map = xcd_map_mode(0);
+  a.xcd_map = xcd_map_mode(1);
   return launch_sparse(a, prob->head_dim, (hipStream_t)stream) == hipSuccess ? ADASPA_OK : ADASPA_ERR_HIP;
 }
 

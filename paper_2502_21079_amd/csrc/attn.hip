@@ -72,6 +72,15 @@ __global__ __launch_bounds__(64 * NW, NW >= 8 ? 1 : 2) void attn_fwd_kernel(Attn
   int skip = -1;              // sparse: entry (relative) holding the ragged block
   bool slow = false;          // sparse: malformed row, take the masked path for all
   const int sub = SPARSE ? a.block / KT : 1;
+  // Sparse: the row's block indices are read 64 at a time into one register
+  // per lane (entry n sits in lane n % 64 of chunk n / 64) and picked out
+  // with readlane; a window of two chunks moves along the row, so no index
+  // load is waited for inside the main loop.
+  auto load_chunk = [&](int c) -> int {
+    const int n = c * 64 + lane;
+    return n < ne ? a.col_idx[e0 + n] : 0;
+  };
+  int c0 = 0, cid0 = 0, cid1 = 0;
   if constexpr (SPARSE) {
     const int64_t r = (int64_t)bh * a.nkb + qt;
     int64_t s = a.row_ptr[r], e = a.row_ptr[r + 1];
@@ -80,22 +89,32 @@ __global__ __launch_bounds__(64 * NW, NW >= 8 ? 1 : 2) void attn_fwd_kernel(Attn
     e0 = (int)s;
     ne = (int)(e - s);
     const bool ragged = L % a.block != 0;
-    for (int i = 0; i < ne; ++i) {
-      const int c = a.col_idx[e0 + i];
-      if (c < 0 || c >= a.nkb) slow = true;
-      else if (ragged && c == a.nkb - 1 && skip < 0) skip = i;
+    for (int c = 0; c * 64 < ne; ++c) {
+      const int n = c * 64 + lane;
+      const int v = load_chunk(c);
+      if (__any(n < ne && (v < 0 || v >= a.nkb))) slow = true;
+      const unsigned long long rb = __ballot(n < ne && ragged && v == a.nkb - 1);
+      if (skip < 0 && rb != 0ull) skip = c * 64 + __builtin_ctzll(rb);
     }
     nf = slow ? 0 : (ne - (skip >= 0 ? 1 : 0)) * sub;
+    cid0 = load_chunk(0);
+    cid1 = load_chunk(1);
   } else {
     nf = L / KT;
   }
+  auto entry = [&](int t) -> int {     // CSR entry of pipeline tile t
+    int i = t / sub;
+    if (skip >= 0 && i >= skip) ++i;
+    return i;
+  };
   auto kbase = [&](int t) -> int {
     if constexpr (!SPARSE) {
       return t * KT;
     } else {
-      int i = t / sub;
-      if (skip >= 0 && i >= skip) ++i;
-      return a.col_idx[e0 + i] * a.block + (t % sub) * KT;
+      const int i = entry(t);
+      const int c = (i >> 6) == c0 ? __builtin_amdgcn_readlane(cid0, i & 63)
+                                   : __builtin_amdgcn_readlane(cid1, i & 63);
+      return c * a.block + (t % sub) * KT;
     }
   };
 
@@ -137,9 +156,24 @@ __global__ __launch_bounds__(64 * NW, NW >= 8 ? 1 : 2) void attn_fwd_kernel(Attn
 #pragma unroll
           for (int e = 0; e < 16; ++e) o[d][e] *= pend_alpha;
       }
+      if constexpr (SPARSE) {
+        // Entries advance by at most two per step and K runs two tiles
+        // ahead of V, so moving on once V leaves chunk c0 keeps both inside
+        // the window; the chunk loaded here is first read ~60 steps later.
+        if ((entry(t) >> 6) > c0) {
+          cid0 = cid1;
+          cid1 = load_chunk(c0 + 2);
+          ++c0;
+        }
+      }
       const bool kload = t + 2 < nf;
       const uint32_t kbyte = kload ? (uint32_t)kbase(t + 2) * (uint32_t)(D * 2) : 0u;
       const uint32_t vbyte = (uint32_t)kbase(t) * (uint32_t)(D * 2);
+      // Re-derived every step: stops the compiler from hoisting one LDS
+      // destination register per load instruction out of the loop (which
+      // overflows the scalar registers); each issue then costs one add.
+      int wv = wave;
+      asm volatile("" : "+s"(wv));
       auto loads = [&](int slot) {
         // Instruction n goes to slot n * NM / NTOT (at most one per slot).
         constexpr int PK = KVLoader<D, NW>::PWK, NTOT = PK + KVLoader<D, NW>::PWV;
@@ -148,9 +182,9 @@ __global__ __launch_bounds__(64 * NW, NW >= 8 ? 1 : 2) void attn_fwd_kernel(Attn
         const int n = (slot * NTOT + NM - 1) / NM;
         if (n >= NTOT || (n * NM) / NTOT != slot) return;
         if (n < PK) {
-          if (kload) ld.k(rK, ldK, kbyte, n, wave);
+          if (kload) ld.k(rK, ldK, kbyte, n, wv);
         } else {
-          ld.v(rV, ldV, vbyte, n - PK, wave);
+          ld.v(rV, ldV, vbyte, n - PK, wv);
         }
       };
       f32x16 s_next[2];
