@@ -71,16 +71,20 @@ __global__ __launch_bounds__(64 * NW, NW >= 8 ? 1 : 2) void attn_fwd_kernel(Attn
   int e0 = 0, ne = 0;         // sparse: CSR entries [e0, e0 + ne)
   int skip = -1;              // sparse: entry (relative) holding the ragged block
   bool slow = false;          // sparse: malformed row, take the masked path for all
-  const int sub = SPARSE ? a.block / KT : 1;
+  constexpr int SUB = SPARSE ? NW / 2 : 1;   // KT-key tiles per sparse block (block = 32 * NW)
+  const int sub = SUB;
   // Sparse: the row's block indices are read 64 at a time into one register
   // per lane (entry n sits in lane n % 64 of chunk n / 64) and picked out
   // with readlane; a window of two chunks moves along the row, so no index
   // load is waited for inside the main loop.
+  // The loads go through a resource bounded to the row, so lanes past its end
+  // read 0 without a branch and each chunk lands directly in its register.
+  __amdgpu_buffer_rsrc_t rC = make_rsrc(a.col_idx, 0u);
   auto load_chunk = [&](int c) -> int {
-    const int n = c * 64 + lane;
-    return n < ne ? a.col_idx[e0 + n] : 0;
+    return __builtin_amdgcn_raw_buffer_load_b32(rC, (uint32_t)(c * 64 + lane) * 4u, 0, 0);
   };
   int c0 = 0, cid0 = 0, cid1 = 0;
+  int skip_at = INT_MAX;      // sparse: pipeline entries at or past it shift by one
   if constexpr (SPARSE) {
     const int64_t r = (int64_t)bh * a.nkb + qt;
     int64_t s = a.row_ptr[r], e = a.row_ptr[r + 1];
@@ -88,6 +92,7 @@ __global__ __launch_bounds__(64 * NW, NW >= 8 ? 1 : 2) void attn_fwd_kernel(Attn
     e = e < s ? s : (e > a.col_count ? a.col_count : e);
     e0 = (int)s;
     ne = (int)(e - s);
+    rC = make_rsrc(a.col_idx + e0, (uint32_t)ne * 4u);
     const bool ragged = L % a.block != 0;
     for (int c = 0; c * 64 < ne; ++c) {
       const int n = c * 64 + lane;
@@ -96,25 +101,25 @@ __global__ __launch_bounds__(64 * NW, NW >= 8 ? 1 : 2) void attn_fwd_kernel(Attn
       const unsigned long long rb = __ballot(n < ne && ragged && v == a.nkb - 1);
       if (skip < 0 && rb != 0ull) skip = c * 64 + __builtin_ctzll(rb);
     }
-    nf = slow ? 0 : (ne - (skip >= 0 ? 1 : 0)) * sub;
+    nf = slow ? 0 : (ne - (skip >= 0 ? 1 : 0)) * SUB;
+    skip_at = skip >= 0 ? skip : INT_MAX;
     cid0 = load_chunk(0);
     cid1 = load_chunk(1);
   } else {
     nf = L / KT;
   }
   auto entry = [&](int t) -> int {     // CSR entry of pipeline tile t
-    int i = t / sub;
-    if (skip >= 0 && i >= skip) ++i;
-    return i;
+    const int i = t / SUB;
+    return i + (i >= skip_at ? 1 : 0);
   };
   auto kbase = [&](int t) -> int {
     if constexpr (!SPARSE) {
       return t * KT;
     } else {
       const int i = entry(t);
-      const int c = (i >> 6) == c0 ? __builtin_amdgcn_readlane(cid0, i & 63)
-                                   : __builtin_amdgcn_readlane(cid1, i & 63);
-      return c * a.block + (t % sub) * KT;
+      const int v0 = __builtin_amdgcn_readlane(cid0, i & 63);
+      const int v1 = __builtin_amdgcn_readlane(cid1, i & 63);
+      return ((i >> 6) == c0 ? v0 : v1) * (SUB * KT) + (t % SUB) * KT;
     }
   };
 
@@ -156,19 +161,22 @@ __global__ __launch_bounds__(64 * NW, NW >= 8 ? 1 : 2) void attn_fwd_kernel(Attn
 #pragma unroll
           for (int e = 0; e < 16; ++e) o[d][e] *= pend_alpha;
       }
+      const bool kload = t + 2 < nf;
+      uint32_t kbyte = kload ? (uint32_t)kbase(t + 2) * (uint32_t)(D * 2) : 0u;
+      uint32_t vbyte = (uint32_t)kbase(t) * (uint32_t)(D * 2);
       if constexpr (SPARSE) {
-        // Entries advance by at most two per step and K runs two tiles
-        // ahead of V, so moving on once V leaves chunk c0 keeps both inside
-        // the window; the chunk loaded here is first read ~60 steps later.
+        // Both entries are read before the window moves, so no read waits
+        // for the chunk load below.  Entries advance by at most two per step
+        // and K runs at most three entries ahead of V, so moving on once V
+        // leaves chunk c0 keeps both inside the window; the chunk loaded
+        // here is first read about 60 steps later.
+        asm volatile("" : "+s"(kbyte), "+s"(vbyte));
         if ((entry(t) >> 6) > c0) {
           cid0 = cid1;
           cid1 = load_chunk(c0 + 2);
           ++c0;
         }
       }
-      const bool kload = t + 2 < nf;
-      const uint32_t kbyte = kload ? (uint32_t)kbase(t + 2) * (uint32_t)(D * 2) : 0u;
-      const uint32_t vbyte = (uint32_t)kbase(t) * (uint32_t)(D * 2);
       // Re-derived every step: stops the compiler from hoisting one LDS
       // destination register per load instruction out of the loop (which
       // overflows the scalar registers); each issue then costs one add.
@@ -317,7 +325,8 @@ __global__ __launch_bounds__(64 * NW, 8 / NW) void block_mass_kernel(MassParams 
   const float sl2 = a.scale_log2;
   // A padding row (past L) gets -inf: exp2 of it is 0 and it adds nothing.
   const float nlse2 = qvalid ? -a.lse[(size_t)bh * L + qrow] * kLog2e : -INFINITY;
-  const int sub = a.block / KT;
+  constexpr int SUB = NW / 2;  // KT-key tiles per block (block = 32 * NW)
+  const int sub = SUB;
   const int nfull = L / KT;   // full key tiles
   float* wrow = a.w + ((size_t)bh * a.nkb + p) * a.nkb;
 
