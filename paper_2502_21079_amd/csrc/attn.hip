@@ -1,11 +1,10 @@
 // Dense and block-sparse flash attention forward (32 query rows per wave) and
 // the block attention-mass search pass, for gfx950.
 //
-// Pipeline.  K/V tiles of 64 keys are double-buffered in LDS and filled by
-// direct global->LDS buffer loads (no register staging); loads for the next
-// tiles are issued before the current tile is computed, so each tile costs one
-// wait and one barrier.  Only a tile that reaches past the end of the sequence
-// pays for key masking.
+// Pipeline.  K/V tiles of 64 keys sit in LDS rings and are filled by direct
+// global->LDS buffer loads (no register staging), issued one or two steps
+// before the tiles are read and spread over the MFMA slots of a step.  Only a
+// tile that reaches past the end of the sequence pays for key masking.
 #include "attn_tile.hpp"
 
 namespace adaspa {
@@ -16,8 +15,7 @@ namespace adaspa {
 // Full key tiles run through a software pipeline: step t computes the scores
 // of tile t+1 (QK MFMAs) and the output update of tile t-1 (PV MFMAs) while
 // the VALU does the softmax of tile t.  K therefore runs one tile ahead of the
-// scores and V one tile behind; each is double-buffered, with the loads of
-// step t landing in the buffers step t-1 finished reading.  A tile that
+// scores and V one tile behind (the K/V rings are described below).  A tile that
 // reaches past the end of the sequence (and, in a malformed sparse row, any
 // out-of-range block) is done afterwards, one at a time with key masking,
 // which keeps the visiting order of the dense and all-blocks sparse paths the
@@ -31,10 +29,13 @@ __global__ __launch_bounds__(64 * NW, NW >= 8 ? 1 : 2) void attn_fwd_kernel(Attn
   constexpr int KS = KDMA::S, VS = VDMA::S;
   constexpr int ND = D / 32;   // 32-wide output column blocks
   constexpr int NK = D / 16;   // MFMA k-steps over the head dimension
-  __shared__ __attribute__((aligned(1024))) u16 sK0[KDMA::ELEMS];
-  __shared__ __attribute__((aligned(1024))) u16 sV0[VDMA::ELEMS];
-  __shared__ __attribute__((aligned(1024))) u16 sK1[KDMA::ELEMS];
-  __shared__ __attribute__((aligned(1024))) u16 sV1[VDMA::ELEMS];
+  // K and V rings of RING tiles.  Tiles are loaded HALF = RING/2 steps before
+  // the step that reads them and the waves meet at a barrier every HALF steps.
+  // Two tiles (a barrier every step) measured faster than four tiles (a
+  // barrier every second step) for the dense kernel on gfx950.
+  constexpr int RING = 2, HALF = RING / 2;
+  __shared__ __attribute__((aligned(1024))) u16 sK[RING][KDMA::ELEMS];
+  __shared__ __attribute__((aligned(1024))) u16 sV[RING][VDMA::ELEMS];
 
   int bh, qt;
   if (a.xcd_map == 2) {
@@ -58,10 +59,11 @@ __global__ __launch_bounds__(64 * NW, NW >= 8 ? 1 : 2) void attn_fwd_kernel(Attn
   const int klane = (c32 * KS + hw) * 8;
 
   // Finite contents everywhere, whatever a bounds-checked load leaves behind.
-  zero_lds<VDMA::SLOTS>(sV0, tid, NT);
-  zero_lds<VDMA::SLOTS>(sV1, tid, NT);
-  zero_lds<KDMA::SLOTS>(sK0, tid, NT);
-  zero_lds<KDMA::SLOTS>(sK1, tid, NT);
+#pragma unroll
+  for (int b = 0; b < RING; ++b) {
+    zero_lds<VDMA::SLOTS>(sV[b], tid, NT);
+    zero_lds<KDMA::SLOTS>(sK[b], tid, NT);
+  }
 
   bf16x8 qf[NK];
   load_q<D>(a.q + hoff, qrow, L, hw, qf);
@@ -132,13 +134,19 @@ __global__ __launch_bounds__(64 * NW, NW >= 8 ? 1 : 2) void attn_fwd_kernel(Attn
   __syncthreads();
 
   if (nf > 0) {
-    KDMA::issue(rK, sK0, kbase(0), wave, lane);
-    if (nf > 1) KDMA::issue(rK, sK1, kbase(1), wave, lane);
+    // Step t reads K(t+1) and V(t-1), so the first steps need K(0..HALF)
+    // and V(0..HALF-2) in place.
+#pragma unroll
+    for (int j = 0; j <= HALF; ++j)
+      if (j < nf) KDMA::issue(rK, sK[j], kbase(j), wave, lane);
+#pragma unroll
+    for (int j = 0; j <= HALF - 2; ++j)
+      if (j < nf) VDMA::issue(rV, sV[j], kbase(j), wave, lane);
     wait_vmem();
     __syncthreads();
     f32x16 s_cur[2];
-    qk_tile<D, KS>(sK0, qf, c32, hw, s_cur);
-    __syncthreads();            // sK0 is refilled by step 0
+    qk_tile<D, KS>(sK[0], qf, c32, hw, s_cur);
+    __syncthreads();            // sK[0] is refilled by step HALF - 1
 
     bf16x8 p_prev[2][2];
 #pragma unroll
@@ -151,19 +159,26 @@ __global__ __launch_bounds__(64 * NW, NW >= 8 ? 1 : 2) void attn_fwd_kernel(Attn
     KVLoader<D, NW> ld;
     ld.init(wave, lane);
 
-    // Step t reads K(t+1) and V(t-1) from buffer (t+1)&1 and loads K(t+2),
-    // V(t) into buffer t&1.  The loads are spread over the MFMA slots of the
-    // step: this wave's K instructions first, then its V instructions.
-    auto step = [&](int t, const u16* rdK, const u16* rdV, u16* ldK, u16* ldV) {
+    // Step t reads K(t+1) and V(t-1) and loads K(t+1+HALF) and V(t-1+HALF)
+    // into the ring slots read HALF steps earlier (tile j lives in slot
+    // j % RING).  A slot is refilled only after the barrier that follows the
+    // step which read it, and a loaded tile is read only after the barrier
+    // that follows its loads.  The loads are spread over the MFMA slots of
+    // the step: this wave's K instructions first, then its V instructions.
+    auto step = [&](int t, auto sync) {
+      const u16* rdK = sK[(t + 1) & (RING - 1)];
+      const u16* rdV = sV[(t - 1) & (RING - 1)];
+      u16* ldK = sK[(t + 1 + HALF) & (RING - 1)];
+      u16* ldV = sV[(t - 1 + HALF) & (RING - 1)];
       if (pend) {
 #pragma unroll
         for (int d = 0; d < ND; ++d)
 #pragma unroll
           for (int e = 0; e < 16; ++e) o[d][e] *= pend_alpha;
       }
-      const bool kload = t + 2 < nf;
-      uint32_t kbyte = kload ? (uint32_t)kbase(t + 2) * (uint32_t)(D * 2) : 0u;
-      uint32_t vbyte = (uint32_t)kbase(t) * (uint32_t)(D * 2);
+      const bool kload = t + 1 + HALF < nf, vload = t - 1 + HALF < nf;
+      uint32_t kbyte = kload ? (uint32_t)kbase(t + 1 + HALF) * (uint32_t)(D * 2) : 0u;
+      uint32_t vbyte = vload ? (uint32_t)kbase(t - 1 + HALF) * (uint32_t)(D * 2) : 0u;
       if constexpr (SPARSE) {
         // Both entries are read before the window moves, so no read waits
         // for the chunk load below.  Entries advance by at most two per step
@@ -192,7 +207,7 @@ __global__ __launch_bounds__(64 * NW, NW >= 8 ? 1 : 2) void attn_fwd_kernel(Attn
         if (n < PK) {
           if (kload) ld.k(rK, ldK, kbyte, n, wv);
         } else {
-          ld.v(rV, ldV, vbyte, n - PK, wv);
+          if (vload) ld.v(rV, ldV, vbyte, n - PK, wv);
         }
       };
       f32x16 s_next[2];
@@ -205,33 +220,35 @@ __global__ __launch_bounds__(64 * NW, NW >= 8 ? 1 : 2) void attn_fwd_kernel(Attn
 #pragma unroll
         for (int s2 = 0; s2 < 2; ++s2) p_prev[g][s2] = p_cur[g][s2];
       }
-      wait_vmem();
-      __syncthreads();
+      if (decltype(sync)::value) {
+        wait_vmem();
+        __syncthreads();
+      }
     };
     int t = 0;
     for (; t + 1 < nf; t += 2) {
-      step(t, sK1, sV1, sK0, sV0);
-      step(t + 1, sK0, sV0, sK1, sV1);
+      step(t, std::integral_constant<bool, HALF == 1>{});
+      step(t + 1, std::true_type{});
     }
-    if (t < nf) step(t, sK1, sV1, sK0, sV0);
+    if (t < nf) step(t, std::true_type{});
     if (pend) {
 #pragma unroll
       for (int d = 0; d < ND; ++d)
 #pragma unroll
         for (int e = 0; e < 16; ++e) o[d][e] *= pend_alpha;
     }
-    pv_tile<ND, VS>(((nf - 1) & 1 ? sV1 : sV0) + voff, p_prev, o);
+    pv_tile<ND, VS>(sV[(nf - 1) & (RING - 1)] + voff, p_prev, o);
     __syncthreads();
   }
 
   // Remaining tiles, one at a time with key masking.
   auto masked_tile = [&](int kb) {
-    KDMA::issue(rK, sK0, kb, wave, lane);
-    VDMA::issue(rV, sV0, kb, wave, lane);
+    KDMA::issue(rK, sK[0], kb, wave, lane);
+    VDMA::issue(rV, sV[0], kb, wave, lane);
     wait_vmem();
     __syncthreads();
     f32x16 s[2];
-    qk_tile<D, KS>(sK0, qf, c32, hw, s);
+    qk_tile<D, KS>(sK[0], qf, c32, hw, s);
     mask_tile(s, L - kb, hw);
     bf16x8 pb[2][2];
     float alpha;
@@ -243,7 +260,7 @@ __global__ __launch_bounds__(64 * NW, NW >= 8 ? 1 : 2) void attn_fwd_kernel(Attn
 #pragma unroll
         for (int e = 0; e < 16; ++e) o[d][e] *= alpha;
     }
-    pv_tile<ND, VS>(sV0 + voff, pb, o);
+    pv_tile<ND, VS>(sV[0] + voff, pb, o);
     __syncthreads();
   };
   if constexpr (SPARSE) {
