@@ -303,6 +303,14 @@ adaspa_status adaspa_block_sparse_attn(const adaspa_problem* prob, const void* q
   a.scale = scale_of(prob);
   a.scale_log2 = a.scale * 1.4426950408889634f;
   a.xcd_map = xcd_map_mode(1);
+  // Text query blocks keep every key block under the text sink, so they are
+  // the longest rows; the kernel starts them first (the result does not
+  // depend on the order).
+  if (prob->text_len > 0) {
+    a.tq0 = prob->text_start / prob->block;
+    a.tq1 = (prob->text_start + prob->text_len + prob->block - 1) / prob->block;
+    if (a.tq1 - a.tq0 >= a.nkb) a.tq0 = a.tq1 = 0;    // every row is text: plain order
+  }
   return launch_sparse(a, prob->head_dim, (hipStream_t)stream) == hipSuccess ? ADASPA_OK : ADASPA_ERR_HIP;
 }
 

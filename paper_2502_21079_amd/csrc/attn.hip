@@ -40,6 +40,8 @@ __global__ __launch_bounds__(64 * NW, NW >= 8 ? 1 : 2) void attn_fwd_kernel(Attn
   int bh, qt;
   if (a.xcd_map == 2) {
     xcd_chunk_map(blockIdx.x, a.nqt, a.batch_heads, bh, qt);
+  } else if (SPARSE && a.xcd_map == 1 && a.tq1 > a.tq0) {
+    text_first_map(blockIdx.x, a.n_wg, a.nqt, a.tq0, a.tq1 - a.tq0, bh, qt);
   } else {
     const int lid = a.xcd_map ? xcd_remap(blockIdx.x, a.n_wg) : (int)blockIdx.x;
     bh = lid / a.nqt;
@@ -278,7 +280,12 @@ __global__ __launch_bounds__(64 * NW, NW >= 8 ? 1 : 2) void attn_fwd_kernel(Attn
   }
 
   // Normalise and store.
-  const float lt = lsum + __shfl_xor(lsum, 32, 64);
+  float lt;
+  {
+    float lo, hi;
+    half_pair(lsum, lo, hi);
+    lt = lo + hi;
+  }
   const float inv = lt > 0.f ? 1.f / lt : 0.f;
   if (qrow < L) {
     u16* orow = a.o + hoff + (size_t)qrow * D;

@@ -213,7 +213,11 @@ __device__ __forceinline__ void softmax_tile(const f32x16 (&s)[2], float& m, flo
   for (int g = 0; g < 2; ++g)
 #pragma unroll
     for (int e = 0; e < 16; e += 2) mt = vmax(mt, vmax(s[g][e], s[g][e + 1]));
-  mt = vmax(mt, __shfl_xor(mt, 32, 64));
+  {
+    float lo, hi;
+    half_pair(mt, lo, hi);
+    mt = vmax(lo, hi);
+  }
   moved = __any(mt > m + thr);
   const float mnew = moved ? fmaxf(m, mt) : m;
   alpha = (mnew == -INFINITY) ? 1.f : fast_exp2((m - mnew) * sl2);
@@ -313,7 +317,7 @@ __device__ __forceinline__ void pipelined_step(Hook&& hook, const u16* klane, co
     }
   };
 
-  float mt = -INFINITY, mtx = -INFINITY, mc = 0.f;
+  float mt = -INFINITY, mtl = -INFINITY, mth = -INFINITY, mc = 0.f;
   const bf16x2 ones = {(__bf16)1.0f, (__bf16)1.0f};
   auto valu = [&](int i) {
     if (i < P1_END) {
@@ -327,9 +331,9 @@ __device__ __forceinline__ void pipelined_step(Hook&& hook, const u16* klane, co
       }
       pin(mt);
     } else if (i == SHFL) {
-      mtx = __shfl_xor(mt, 32, 64);
+      half_pair(mt, mtl, mth);
     } else if (i == MC) {
-      mt = vmax(mt, mtx);
+      mt = vmax(mtl, mth);
       moved = __any(mt > m + thr);
       const float mnew = moved ? fmaxf(m, mt) : m;
       alpha = (mnew == -INFINITY) ? 1.f : fast_exp2((m - mnew) * sl2);

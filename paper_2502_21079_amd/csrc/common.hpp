@@ -68,6 +68,16 @@ __device__ __forceinline__ void xcd_chunk_map(int bid, int nqt, int nbh, int& bh
   qt = c0 + rel % sz;
 }
 
+// Lane l's value and lane (l ^ 32)'s value, returned as (a, b) in an order
+// that depends on the half-wave: a = v[l & 31], b = v[(l & 31) + 32].  One
+// v_permlane32_swap (a VALU op; no LDS round trip as with a shuffle).
+__device__ __forceinline__ void half_pair(float v, float& a, float& b) {
+  const unsigned u = __float_as_uint(v);
+  const auto r = __builtin_amdgcn_permlane32_swap(u, u, false, false);
+  a = __uint_as_float(r[0]);
+  b = __uint_as_float(r[1]);
+}
+
 // Sum over the 64 lanes of a wave, returned to every lane.  DPP moves sum
 // within each row of 16 lanes (no LDS round trips); the four row sums are
 // then read out and added in a fixed order, so the result is deterministic.
@@ -76,6 +86,31 @@ __device__ __forceinline__ float dpp_plus(float v) {
   const int moved = __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, v), CTRL, 0xF, 0xF, false);
   return v + __builtin_bit_cast(float, moved);
 }
+// Long rows first: the nt = ntq * nbh workgroups of the ntq query tiles
+// [tq0, tq0 + ntq) of every head are dispatched first (hardware ids 0..nt-1,
+// spread round-robin over the XCDs), and the other tiles follow with each XCD
+// receiving one contiguous range of the remaining (head, tile) order, as in
+// xcd_remap.  In block-sparse attention the text query blocks keep every key
+// block, so they are the longest rows by far; starting them first removes the
+// tail they would otherwise leave.  Bijective for any sizes.
+__device__ __forceinline__ void text_first_map(int hid, int n, int nqt, int tq0, int ntq, int& bh,
+                                               int& qt) {
+  const int nt = ntq * (n / nqt);
+  if (hid < nt) {
+    bh = hid / ntq;
+    qt = tq0 + hid % ntq;
+    return;
+  }
+  auto cnt = [](int N, int y) { return N > y ? (N + 7 - y) / 8 : 0; };   // ids < N on XCD y
+  const int x = hid % 8;
+  int lid = cnt(hid, x) - cnt(nt, x);
+  for (int y = 0; y < x; ++y) lid += cnt(n, y) - cnt(nt, y);
+  const int nvq = nqt - ntq;
+  bh = lid / nvq;
+  const int r = lid % nvq;
+  qt = r < tq0 ? r : r + ntq;
+}
+
 __device__ __forceinline__ float wave_sum(float v) {
   v = dpp_plus<0xB1>(v);    // quad_perm [1,0,3,2]: pairs
   v = dpp_plus<0x4E>(v);    // quad_perm [2,3,0,1]: quads

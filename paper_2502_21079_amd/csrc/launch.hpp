@@ -26,6 +26,7 @@ struct AttnParams {
   float scale;
   float scale_log2;           // scale * log2(e)
   int xcd_map;                // 0 hardware order, 1 contiguous per XCD, 2 head-chunked
+  int tq0, tq1;               // sparse: text query blocks [tq0, tq1), dispatched first
 };
 
 struct MassParams {
