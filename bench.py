@@ -149,6 +149,7 @@ def amortised_loop(w, tau, steps: int = 50, drift: float = 0.05, research_at: in
     0 (Algorithm 2, no dense pass) and later steps use the new pattern; its
     per-step error is reported for those steps."""
     B, H, L, D, blk = w.batch, w.heads, w.seqlen, w.head_dim, w.block
+    txt = {"text_start": w.text_start, "text_len": w.text_len}
     x0 = make_qkv(w, device="cuda", fp32=True)
     eps = make_drift_noise(w, device="cuda", seed=4)
     xt = [torch.empty(B, H, L, D, dtype=torch.bfloat16, device="cuda") for _ in range(3)]
@@ -172,7 +173,7 @@ def amortised_loop(w, tau, steps: int = 50, drift: float = 0.05, research_at: in
             per_step.append({"t": 0, "path": "dense"})
             continue
         timer("sparse", ad.block_sparse_attn, q, k, v, res.row_ptr, res.col_idx, block=blk,
-              out=sp_out, want_lse=False)
+              out=sp_out, want_lse=False, **txt)
         ad.dense_attn_lse(q, k, v, out=dense_out, want_lse=False)     # reference, untimed
         rec = {"t": t, **err_stats(sp_out, dense_out)}
         if t == research_at:
@@ -181,7 +182,7 @@ def amortised_loop(w, tau, steps: int = 50, drift: float = 0.05, research_at: in
                          head_param_bp=tau)
         if t >= research_at:
             timer("sparse_phase2", ad.block_sparse_attn, q, k, v, res2.row_ptr, res2.col_idx,
-                  block=blk, out=sp_out, want_lse=False)
+                  block=blk, out=sp_out, want_lse=False, **txt)
             rec["two_phase"] = err_stats(sp_out, dense_out)
         per_step.append(rec)
     ev = timer.collect()
@@ -253,6 +254,7 @@ def main():
     w = LONG
     B, H, L, D, blk = w.batch, w.heads, w.seqlen, w.head_dim, w.block
     nb = w.nblocks
+    txt = {"text_start": w.text_start, "text_len": w.text_len}
     print(f"[bench] generating {w.name}", file=sys.stderr, flush=True)
     q, k, v = make_qkv(w, device="cuda")
     out = torch.empty_like(q)
@@ -272,7 +274,8 @@ def main():
                     text_len=w.text_len, mode="coverage", head_param_bp=tau, workspace=ws)
         if args.kernel in ("all", "sparse"):
             rp, ci = step.pattern if res is None else (res.row_ptr, res.col_idx)
-            t("sparse", ad.block_sparse_attn, q, k, v, rp, ci, block=blk, out=sp_out, want_lse=False)
+            t("sparse", ad.block_sparse_attn, q, k, v, rp, ci, block=blk, out=sp_out, want_lse=False,
+              **txt)
         return res
 
     # pattern for a sparse-only profile run
@@ -338,10 +341,11 @@ def main():
                                 scores=res.block_mass, shape=(B, H, L, D))
             tm = Timer()
             for _ in range(2):
-                ad.block_sparse_attn(q, k, v, r.row_ptr, r.col_idx, block=blk, out=sp_out, want_lse=False)
+                ad.block_sparse_attn(q, k, v, r.row_ptr, r.col_idx, block=blk, out=sp_out, want_lse=False,
+                                     **txt)
             for _ in range(max(3, args.steps)):
                 tm("s", ad.block_sparse_attn, q, k, v, r.row_ptr, r.col_idx, block=blk, out=sp_out,
-                   want_lse=False)
+                   want_lse=False, **txt)
             ms = float(np.mean(tm.collect()["s"]))
             nz = r.nnz()
             hk = r.head_k.cpu().numpy()[0].astype(np.float64)

@@ -166,7 +166,9 @@ adaspa_status adaspa_block_search(const adaspa_problem* prob, const void* q,
  * the number of readable col_idx entries: row bounds are clamped to
  * [0, col_count] and entries outside [0, NB) are skipped, so malformed
  * patterns never read out of bounds.  Rows should be strictly ascending
- * (a repeated block would be counted twice). */
+ * (a repeated block would be counted twice).  prob->text_start/text_len only
+ * order the work (the text query blocks, which keep every key block under the
+ * text sink, are started first); the results do not depend on them. */
 adaspa_status adaspa_block_sparse_attn(const adaspa_problem* prob, const void* q,
                                        const void* k, const void* v,
                                        const int32_t* row_ptr,

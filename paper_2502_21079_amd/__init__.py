@@ -236,8 +236,10 @@ def block_search(q, k, lse, *, block: int, text_start: int, text_len: int,
 
 
 def block_sparse_attn(q, k, v, row_ptr, col_idx, *, block: int, scale: Optional[float] = None,
-                      out=None, lse=None, want_lse: bool = True):
-    """Blockified sparse attention over the CSR key-block lists.  Returns (out, lse)."""
+                      out=None, lse=None, want_lse: bool = True, text_start: int = 0,
+                      text_len: int = 0):
+    """Blockified sparse attention over the CSR key-block lists.  Returns (out, lse).
+    ``text_start``/``text_len`` only order the work (text query blocks first)."""
     _check_qkv(q, k, v)
     lib = load_library()
     B, H, L, D = q.shape
@@ -251,7 +253,7 @@ def block_sparse_attn(q, k, v, row_ptr, col_idx, *, block: int, scale: Optional[
         out = torch.empty_like(q)
     if lse is None and want_lse:
         lse = torch.empty(B, H, L, dtype=torch.float32, device=q.device)
-    prob = _problem(q, block, 0, 0, scale)
+    prob = _problem(q, block, text_start, text_len, scale)
     _check(lib.adaspa_block_sparse_attn(ctypes.byref(prob), _ptr(q), _ptr(k), _ptr(v),
                                         _ptr(row_ptr), _ptr(col_idx), int(col_idx.numel()),
                                         _ptr(out), _ptr(lse), _stream(q.device)))

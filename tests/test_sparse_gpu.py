@@ -108,3 +108,35 @@ def test_sparse_deterministic():
     o2, l2 = ad.block_sparse_attn(q, k, v, rp, ci, block=128)
     torch.cuda.synchronize()
     assert torch.equal(o1, o2) and torch.equal(l1, l2)
+
+
+@pytest.mark.parametrize("text", [(0, 128), (512, 200), (1664, 384), (0, 0)])
+def test_text_first_order_covers_every_row(text):
+    """The work order that starts text query blocks first is a bijection:
+    every (head, query block) row is computed, for text at the start, in the
+    middle (unaligned), at the end and absent, with more heads than XCDs."""
+    t0, tl = text
+    w = TINY.replace(heads=9, block=128)
+    q, k, v = make_qkv(w, device="cuda")
+    nb = w.nblocks
+    tb = text_blocks(w.seqlen, w.block, t0, tl) if tl > 0 else []
+    # text query blocks keep every block (as the selection emits them); others keep 3
+    lists = []
+    g = np.random.default_rng(7)
+    for r in range(w.heads * nb):
+        p = r % nb
+        if p in tb:
+            lists.append(list(range(nb)))
+        else:
+            lists.append(sorted(set(tb) | set(g.choice(nb, 3, replace=False).tolist())))
+    rp = torch.tensor([0] + list(np.cumsum([len(x) for x in lists])), dtype=torch.int32)
+    ci = torch.tensor([c for x in lists for c in x], dtype=torch.int32)
+    out, lse = ad.block_sparse_attn(q, k, v, rp.cuda(), ci.cuda(), block=w.block, text_start=t0,
+                                    text_len=tl)
+    torch.cuda.synchronize()
+    rpn, cin = rp.numpy(), ci.numpy()
+    for h in range(w.heads):
+        o_ref, l_ref = oracle.block_sparse_attention(f64(q[0, h]), f64(k[0, h]), f64(v[0, h]),
+                                                     rpn[h * nb:(h + 1) * nb + 1], cin, w.scale, w.block)
+        check_out(out[0, h], o_ref, f"h{h}")
+        check_lse(lse[0, h], l_ref)
