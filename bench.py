@@ -227,6 +227,8 @@ def main():
                     help="with --kernel sparse: per-head keep fraction (basis points, TOPK) "
                          "instead of the coverage selection")
     ap.add_argument("--no-cpu", action="store_true")
+    ap.add_argument("--block", type=int, choices=[64, 128], default=LONG.block,
+                    help="sparse block size (the paper's default is 64; the 110K workload uses 128)")
     ap.add_argument("--no-amortised", action="store_true",
                     help="skip the 50-step denoising-loop workload")
     ap.add_argument("--kernel", choices=["all", "dense", "sparse", "search", "copy"], default="all",
@@ -251,7 +253,7 @@ def main():
         print(f"[bench] copied {src.numel() * 2} bytes x {max(1, args.steps)}", file=sys.stderr, flush=True)
         return
 
-    w = LONG
+    w = LONG if args.block == LONG.block else LONG.replace(block=args.block, name=LONG.name.replace("_b128", f"_b{args.block}"))
     B, H, L, D, blk = w.batch, w.heads, w.seqlen, w.head_dim, w.block
     nb = w.nblocks
     txt = {"text_start": w.text_start, "text_len": w.text_len}
