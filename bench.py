@@ -215,6 +215,45 @@ def amortised_loop(w, tau, steps: int = 50, drift: float = 0.05, research_at: in
             "two_phase_schedule": two_phase, "per_step": per_step}
 
 
+def length_sweep(block: int, keep_bp: int = 1000, seconds=(4, 8, 12, 16, 24), reps: int = 2):
+    """Attention-only scaling: dense vs. block-sparse attention across 720p
+    clip lengths (4 latent frames per second of 3,440 patches, 256 text
+    tokens, 24 heads, d = 128), at sparsity 0.9 (TOPK keep 10% with the text
+    sink) chosen from the block masses of the fresh LSE.  Speedup = dense ms /
+    sparse ms; the search (mass + selection) is timed beside them."""
+    rows = []
+    for sec in seconds:
+        w = LONG.replace(frames=4 * sec, seqlen=LONG.text_len + 4 * sec * LONG.patches, block=block,
+                         name=f"sweep_{sec}s")
+        B, H, L, D = w.batch, w.heads, w.seqlen, w.head_dim
+        print(f"[bench] length sweep {sec} s: L={L}, block {block}", file=sys.stderr, flush=True)
+        q, k, v = make_qkv(w, device="cuda")
+        out = torch.empty_like(q)
+        lse = torch.empty(B, H, L, dtype=torch.float32, device="cuda")
+        txt = {"text_start": w.text_start, "text_len": w.text_len}
+        timer = Timer()
+        res = None
+        for it in range(reps + 1):
+            tm = timer if it > 0 else Timer()
+            tm("dense", ad.dense_attn_lse, q, k, v, out=out, lse=lse)
+            res = tm("search", ad.block_search, q, k, lse, block=block, text_start=w.text_start,
+                     text_len=w.text_len, mode="topk", head_param_bp=[keep_bp] * H)
+            tm("sparse", ad.block_sparse_attn, q, k, v, res.row_ptr, res.col_idx, block=block,
+               out=out, want_lse=False, **txt)
+        torch.cuda.synchronize()
+        ev = {kname: float(np.mean(v_)) for kname, v_ in timer.collect().items()}
+        nnz = res.nnz()
+        rows.append({"seconds": sec, "seq_len": L, "nblocks": w.nblocks, "dense_ms": round(ev["dense"], 3),
+                     "search_ms": round(ev["search"], 3), "sparse_ms": round(ev["sparse"], 3),
+                     "density": round(nnz / (B * H * w.nblocks ** 2), 5),
+                     "sparse_tflops": round(sparse_flops(nnz, block, D) / (ev["sparse"] * 1e-3) / 1e12, 1),
+                     "speedup_vs_dense": round(ev["dense"] / ev["sparse"], 3),
+                     "speedup_incl_search": round(ev["dense"] / (ev["sparse"] + ev["search"]), 3)})
+        del q, k, v, out, lse, res
+        torch.cuda.empty_cache()
+    return rows
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -227,6 +266,8 @@ def main():
                     help="with --kernel sparse: per-head keep fraction (basis points, TOPK) "
                          "instead of the coverage selection")
     ap.add_argument("--no-cpu", action="store_true")
+    ap.add_argument("--length-sweep", action="store_true",
+                    help="attention-only scaling sweep over 4-24 s clips (prints its own JSON line)")
     ap.add_argument("--block", type=int, choices=[64, 128], default=LONG.block,
                     help="sparse block size (the paper's default is 64; the 110K workload uses 128)")
     ap.add_argument("--no-amortised", action="store_true",
@@ -244,6 +285,12 @@ def main():
         sys.exit(2)
     assert torch.cuda.is_available(), "bench.py needs a GPU"
     ad.load_library()
+    if args.length_sweep:
+        rows = length_sweep(args.block)
+        print(json.dumps({"metric": "attention-only scaling sweep (dense vs block-sparse, sparsity 0.9)",
+                          "unit": "ms", "block": args.block, "heads": LONG.heads, "head_dim": LONG.head_dim,
+                          "data": "synthetic", "rows": rows}), flush=True)
+        return
     if args.kernel == "copy":
         src = torch.empty(1 << 29, dtype=torch.int16, device="cuda").fill_(1)   # 1 GiB
         dst = torch.empty_like(src)

@@ -145,6 +145,8 @@ int64_t adaspa_block_search_capacity(const adaspa_problem* prob,
  * cap = floor(2^62 / (NB*NB)) (NaN and m <= 0 give 0); coverage holds when
  * kept * 10000 >= total * tau_bp; recall = (float)((double)kept/(double)total),
  * 1 when total is 0.
+ * Supported: NB <= 8192 key blocks, H <= 512 heads and B*H*NB*NB < 2^31
+ * (ADASPA_ERR_UNSUPPORTED otherwise).
  * q, k, lse may be NULL with ADASPA_F_SCORES_GIVEN.  col_capacity must be at
  * least adaspa_block_search_capacity(); workspace must hold
  * adaspa_block_search_workspace() bytes, 256-byte aligned. */

@@ -306,16 +306,20 @@ __global__ __launch_bounds__(64 * NW, NW >= 8 ? 1 : 2) void attn_fwd_kernel(Attn
 // ---------------------------------------------------------------------------
 // Block attention mass: W[p][c] = sum_{i in p, j in c} exp(scale*q_i.k_j - LSE_i)
 //
-// One workgroup per query block p (32 rows per wave).  Full key tiles run
-// through a software pipeline: step t forms the scores of tile t+1 (QK MFMAs)
-// while the VALU exponentiates and sums tile t; K is double-buffered and the
-// loads of tile t+2 are spread over the step.  Per-wave sums of a finished
-// key block are combined in a fixed order into an LDS ring of row p, which
-// is written out 64 blocks at a time (coalesced).
+// One workgroup of four waves (32 rows each) covers 128 query rows: one query
+// block of 128 or two adjacent query blocks of 64 (QB), so every K tile
+// brought into LDS serves 128 rows either way.  Full key tiles run through a
+// software pipeline: step t forms the scores of tile t+1 (QK MFMAs) while the
+// VALU exponentiates and sums tile t; K is double-buffered and the loads of
+// tile t+2 are spread over the step.  Per-wave sums of a finished key block
+// are combined in a fixed order into an LDS ring per query block, which is
+// written out 64 blocks at a time (coalesced).
 // ---------------------------------------------------------------------------
-template <int D, int NW>
-__global__ __launch_bounds__(64 * NW, 8 / NW) void block_mass_kernel(MassParams a) {
-  constexpr int NT = 64 * NW;
+template <int D, int QB>
+__global__ __launch_bounds__(256, 2) void block_mass_kernel(MassParams a) {
+  constexpr int NW = 4, NT = 64 * NW;
+  constexpr int WPB = NW / QB;       // waves per query block
+  constexpr int SUB = 2 / QB;        // KT-key tiles per key block (block = 128 / QB)
   using KDMA = TileDMA<D, NW, 1>;
   constexpr int KS = KDMA::S;
   constexpr int NK = D / 16;
@@ -323,23 +327,25 @@ __global__ __launch_bounds__(64 * NW, 8 / NW) void block_mass_kernel(MassParams 
   __shared__ __attribute__((aligned(1024))) u16 sK1[KDMA::ELEMS];
   constexpr int RING = 128, CHUNK = 64;
   __shared__ float sRed[2][NW];     // per-wave sums of the last two blocks
-  __shared__ float sW[RING];        // blocks of row p not yet written out
+  __shared__ float sW[QB][RING];    // blocks of the QB rows of W not yet written out
 
-  int bh, p;
+  const int ngrp = (a.nkb + QB - 1) / QB;    // query-block groups per head
+  int bh, pg;
   if (a.xcd_map == 2) {
-    xcd_chunk_map(blockIdx.x, a.nkb, a.batch_heads, bh, p);
+    xcd_chunk_map(blockIdx.x, ngrp, a.batch_heads, bh, pg);
   } else {
     const int lid = a.xcd_map ? xcd_remap(blockIdx.x, a.n_wg) : (int)blockIdx.x;
-    bh = lid / a.nkb;
-    p = lid % a.nkb;
+    bh = lid / ngrp;
+    pg = lid % ngrp;
   }
+  const int p0 = pg * QB;           // first query block of the group
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);   // wave-uniform
   const int hw = lane >> 5, c32 = lane & 31;
   const int L = a.seqlen;
   const size_t hoff = (size_t)bh * L * D;
   const __amdgpu_buffer_rsrc_t rK = make_rsrc(a.k + hoff, (uint32_t)L * D * 2u);
-  const int qrow = p * a.block + wave * 32 + c32;   // block = 32 * NW
+  const int qrow = pg * 128 + wave * 32 + c32;
   const bool qvalid = qrow < L;
 
   zero_lds<KDMA::SLOTS>(sK0, tid, NT);
@@ -349,10 +355,10 @@ __global__ __launch_bounds__(64 * NW, 8 / NW) void block_mass_kernel(MassParams 
   const float sl2 = a.scale_log2;
   // A padding row (past L) gets -inf: exp2 of it is 0 and it adds nothing.
   const float nlse2 = qvalid ? -a.lse[(size_t)bh * L + qrow] * kLog2e : -INFINITY;
-  constexpr int SUB = NW / 2;  // KT-key tiles per block (block = 32 * NW)
   const int sub = SUB;
   const int nfull = L / KT;   // full key tiles
-  float* wrow = a.w + ((size_t)bh * a.nkb + p) * a.nkb;
+  float* wrow = a.w + ((size_t)bh * a.nkb + p0) * a.nkb;    // row p0 + qb at wrow + qb * nkb
+  const int nrows = a.nkb - p0 < QB ? a.nkb - p0 : QB;      // rows of W this group owns
 
   float acc = 0.f;
   auto finish_block = [&](int blk) {
@@ -363,10 +369,13 @@ __global__ __launch_bounds__(64 * NW, 8 / NW) void block_mass_kernel(MassParams 
   // After a barrier: waves combined in a fixed order (deterministic).
   auto publish = [&](int blk) {
     if (tid == 0) {
-      float v = 0.f;
 #pragma unroll
-      for (int w = 0; w < NW; ++w) v += sRed[blk & 1][w];
-      sW[blk % RING] = v;
+      for (int qb = 0; qb < QB; ++qb) {
+        float v = 0.f;
+#pragma unroll
+        for (int w = qb * WPB; w < (qb + 1) * WPB; ++w) v += sRed[blk & 1][w];
+        sW[qb][blk % RING] = v;
+      }
     }
   };
   // After a barrier that follows the publication of block blk: once a chunk
@@ -375,7 +384,10 @@ __global__ __launch_bounds__(64 * NW, 8 / NW) void block_mass_kernel(MassParams 
   int flushed = 0;                  // blocks [0, flushed) written out
   auto flush = [&](int done) {      // blocks [0, done) published
     while (done - flushed >= CHUNK) {
-      if (tid < CHUNK) wrow[flushed + tid] = sW[(flushed + tid) % RING];
+      if (tid < CHUNK * QB) {
+        const int qb = tid / CHUNK, i = flushed + tid % CHUNK;
+        if (qb < nrows) wrow[(size_t)qb * a.nkb + i] = sW[qb][i % RING];
+      }
       flushed += CHUNK;
     }
   };
@@ -453,7 +465,8 @@ __global__ __launch_bounds__(64 * NW, 8 / NW) void block_mass_kernel(MassParams 
     publish(a.nkb - 1);
   }
   __syncthreads();
-  for (int i = flushed + tid; i < a.nkb; i += NT) wrow[i] = sW[i % RING];
+  for (int qb = 0; qb < nrows; ++qb)
+    for (int i = flushed + tid; i < a.nkb; i += NT) wrow[(size_t)qb * a.nkb + i] = sW[qb][i % RING];
 }
 
 // ---------------------------------------------------------------------------
@@ -488,20 +501,21 @@ hipError_t launch_sparse(AttnParams a, int D, hipStream_t st) {
   return launch_attn<128, 4, true>(a, st);
 }
 
-template <int D, int NW>
-static hipError_t launch_mass_t(const MassParams& a, hipStream_t st) {
-  hipLaunchKernelGGL((block_mass_kernel<D, NW>), dim3(a.n_wg), dim3(64 * NW), 0, st, a);
+template <int D, int QB>
+static hipError_t launch_mass_t(MassParams a, hipStream_t st) {
+  a.n_wg = (a.nkb + QB - 1) / QB * a.batch_heads;
+  hipLaunchKernelGGL((block_mass_kernel<D, QB>), dim3(a.n_wg), dim3(256), 0, st, a);
   return hipGetLastError();
 }
 
 hipError_t launch_block_mass(MassParams a, int D, hipStream_t st) {
-  a.n_wg = a.nkb * a.batch_heads;
+  // 128 query rows per workgroup: two query blocks of 64 or one of 128.
   if (a.block == 64) {
     if (D == 64) return launch_mass_t<64, 2>(a, st);
     return launch_mass_t<128, 2>(a, st);
   }
-  if (D == 64) return launch_mass_t<64, 4>(a, st);
-  return launch_mass_t<128, 4>(a, st);
+  if (D == 64) return launch_mass_t<64, 1>(a, st);
+  return launch_mass_t<128, 1>(a, st);
 }
 
 }  // namespace adaspa

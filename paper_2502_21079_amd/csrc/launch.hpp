@@ -44,7 +44,7 @@ struct MassParams {
 };
 
 constexpr int kMaxHeads = 512;
-constexpr int kMaxBlocks = 4096;
+constexpr int kMaxBlocks = 8192;
 
 struct SelectParams {
   const float* w;             // [R, nb] masses, R = B*H*nb rows

@@ -53,7 +53,7 @@ __device__ int64_t block_exclusive_scan(int64_t v, int64_t* sh, int64_t* total) 
 // the order and the running exact sums.  Text query rows keep everything:
 // their running sum is the row total at every position.
 __global__ __launch_bounds__(SEL_NT) void select_rank_kernel(SelectParams P) {
-  __shared__ uint64_t keys[kMaxBlocks];
+  extern __shared__ uint64_t keys[];    // next power of two >= nb entries (launch size)
   __shared__ int64_t scan[SEL_NT];
   const int row = blockIdx.x;
   const int tid = threadIdx.x;
@@ -104,24 +104,26 @@ __global__ __launch_bounds__(SEL_NT) void select_rank_kernel(SelectParams P) {
       __syncthreads();
     }
   }
-  // Running exact sums in sorted order (thread chunks are contiguous).
-  int64_t vals[kMaxBlocks / SEL_NT];
+  // Running exact sums in sorted order (thread chunks are contiguous): each
+  // thread sums its chunk, the chunk offsets come from a block scan, and a
+  // second pass over the chunk writes the running sums.
   int64_t s = 0;
   for (int u = 0; u < per; ++u) {
     int i = tid * per + u;
-    int64_t v = 0;
     if (i < nb) {
       int idx = 0x7FFFFFFF - (int)(keys[i] & 0x7FFFFFFFull);
       ord[i] = idx;
-      v = q32(w[idx], P.cap);
+      s += q32(w[idx], P.cap);
     }
-    s += v;
-    vals[u] = s;
   }
-  int64_t off = block_exclusive_scan(s, scan, nullptr);
+  int64_t run = block_exclusive_scan(s, scan, nullptr);
   for (int u = 0; u < per; ++u) {
     int i = tid * per + u;
-    if (i < nb) pref[i] = off + vals[u];
+    if (i < nb) {
+      int idx = 0x7FFFFFFF - (int)(keys[i] & 0x7FFFFFFFull);
+      run += q32(w[idx], P.cap);
+      pref[i] = run;
+    }
   }
 }
 
@@ -238,7 +240,9 @@ __global__ __launch_bounds__(SEL_NT) void select_emit_kernel(SelectParams P) {
 
 hipError_t launch_select(const SelectParams& P, hipStream_t st) {
   const int rows = P.batch_heads * P.nb;
-  hipLaunchKernelGGL(select_rank_kernel, dim3(rows), dim3(SEL_NT), 0, st, P);
+  int n = 1;
+  while (n < P.nb) n <<= 1;
+  hipLaunchKernelGGL(select_rank_kernel, dim3(rows), dim3(SEL_NT), (size_t)n * sizeof(uint64_t), st, P);
   hipLaunchKernelGGL(select_curve_kernel, dim3((P.nb + SEL_NT - 1) / SEL_NT, P.batch_heads),
                      dim3(SEL_NT), 0, st, P);
   hipLaunchKernelGGL(select_heads_kernel, dim3(1), dim3(SEL_NT), 0, st, P);

@@ -110,6 +110,14 @@ def test_hierarchical_capacity_and_validation(lib):
         assert lib.adaspa_block_search_capacity(ctypes.byref(p), ctypes.byref(s)) == -1
 
 
+def test_block_count_limit(lib):
+    s, _a = _sel(mode=0, params=(1000,))
+    ok = _prob(seqlen=8192 * 64, heads=1, block=64, text_len=256)
+    assert lib.adaspa_block_search_capacity(ctypes.byref(ok), ctypes.byref(s)) > 0
+    too_many = _prob(seqlen=8192 * 64 + 1, heads=1, block=64, text_len=256)
+    assert lib.adaspa_block_search_capacity(ctypes.byref(too_many), ctypes.byref(s)) == -1
+
+
 def test_capacity_matches_oracle_counts(lib):
     import oracle
     for keep in (0, 1, 500, 1000, 2000, 5000, 10000):

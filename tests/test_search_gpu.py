@@ -126,6 +126,20 @@ def test_selection_bit_exact_given_scores(case, mode, ties):
     _compare_selection(res, sel)
 
 
+def test_selection_bit_exact_many_blocks():
+    """More than 4,096 key blocks (block 64 at a 266K-token clip): the rank
+    kernel's key buffer is sized per launch and reaches its largest size."""
+    B, H, block = 1, 1, 64
+    nb = 4160
+    L = nb * block
+    W = random_block_masses((B, H, nb, nb), seed=77)
+    res = ad.block_search(None, None, None, block=block, text_start=0, text_len=256, mode="topk",
+                          head_param_bp=[1000], scores=W.cuda(), shape=(B, H, L, 64))
+    torch.cuda.synchronize()
+    sel = oracle.select_blocks(W.numpy(), L, block, 0, 256, "topk", [1000])
+    _compare_selection(res, sel)
+
+
 def test_selection_extremes_given_scores():
     B, H, L, block = 1, 4, 2048, 64
     nb = 32
