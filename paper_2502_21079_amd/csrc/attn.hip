@@ -304,6 +304,321 @@ __global__ __launch_bounds__(64 * NW, NW >= 8 ? 1 : 2) void attn_fwd_kernel(Attn
 }
 
 // ---------------------------------------------------------------------------
+// Block-sparse attention with block 64, two query blocks per workgroup.
+//
+// Four waves cover query blocks 2P (waves 0-1) and 2P+1 (waves 2-3), 128
+// rows, and walk the sorted union of the two rows' key-block lists through
+// the same pipeline as attn_fwd_kernel (one 64-key tile per block).  For a
+// tile that only one row keeps, the other half's scores are set to -inf, so
+// its probabilities are exact zeros: each half accumulates exactly its own
+// tiles, in ascending order, as a one-block workgroup would.  Neighbouring
+// query blocks keep mostly the same key blocks, so the union is little larger
+// than each list, and every tile brought into LDS serves 128 rows.  Rows
+// must be strictly ascending lists of blocks in [0, NB); otherwise (or for
+// the ragged last block) tiles are done one at a time with key masking.
+// ---------------------------------------------------------------------------
+template <int D>
+__global__ __launch_bounds__(256, 2) void attn_sparse_pair_kernel(AttnParams a) {
+  constexpr int NW = 4, NT = 256;
+  using KDMA = TileDMA<D, NW, 1>;
+  using VDMA = TileDMA<D, NW, 2>;
+  constexpr int KS = KDMA::S, VS = VDMA::S;
+  constexpr int ND = D / 32;
+  constexpr int NK = D / 16;
+  static_assert(VDMA::ELEMS * 2 >= kMaxBlocks, "the V slot holds the block map");
+  __shared__ __attribute__((aligned(1024))) u16 sK[2][KDMA::ELEMS];
+  __shared__ __attribute__((aligned(1024))) u16 sV[2][VDMA::ELEMS];
+
+  int bh, pq;
+  if (a.xcd_map == 1 && a.tq1 > a.tq0) {
+    text_first_map(blockIdx.x, a.n_wg, a.nqt, a.tq0, a.tq1 - a.tq0, bh, pq);
+  } else {
+    const int lid = a.xcd_map ? xcd_remap(blockIdx.x, a.n_wg) : (int)blockIdx.x;
+    bh = lid / a.nqt;
+    pq = lid % a.nqt;
+  }
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);   // wave-uniform
+  const int mybit = 1 << (wave >> 1);                          // 1: row 2P, 2: row 2P+1
+  const int hw = lane >> 5, c32 = lane & 31;
+  const int gi = lane & 15, grp = lane >> 4;
+  const int L = a.seqlen, nkb = a.nkb;
+  const size_t hoff = (size_t)bh * L * D;
+  const uint32_t hbytes = (uint32_t)L * D * 2u;
+  const __amdgpu_buffer_rsrc_t rK = make_rsrc(a.k + hoff, hbytes);
+  const __amdgpu_buffer_rsrc_t rV = make_rsrc(a.v + hoff, hbytes);
+  const int qrow = pq * 128 + wave * 32 + c32;
+  const int voff = ((4 * hw + (gi >> 2)) * VS) * 8 + 16 * (grp & 1) + 4 * (gi & 3);
+  const int klane = (c32 * KS + hw) * 8;
+
+#pragma unroll
+  for (int b = 0; b < 2; ++b) {
+    zero_lds<VDMA::SLOTS>(sV[b], tid, NT);
+    zero_lds<KDMA::SLOTS>(sK[b], tid, NT);
+  }
+  bf16x8 qf[NK];
+  load_q<D>(a.q + hoff, qrow, L, hw, qf);
+
+  // The two rows.  Each row's indices are read 64 at a time into one
+  // register per lane through a resource bounded to the row (lanes past its
+  // end read 0), as in attn_fwd_kernel.
+  int len[2], beg[2];
+#pragma unroll
+  for (int r = 0; r < 2; ++r) {
+    const int p = 2 * pq + r;
+    int64_t s0 = 0, e0 = 0;
+    if (p < nkb) {
+      const int64_t row = (int64_t)bh * nkb + p;
+      s0 = a.row_ptr[row];
+      e0 = a.row_ptr[row + 1];
+      s0 = s0 < 0 ? 0 : (s0 > a.col_count ? a.col_count : s0);
+      e0 = e0 < s0 ? s0 : (e0 > a.col_count ? a.col_count : e0);
+    }
+    beg[r] = (int)s0;
+    len[r] = (int)(e0 - s0);
+  }
+  const __amdgpu_buffer_rsrc_t rC0 = make_rsrc(a.col_idx + beg[0], (uint32_t)len[0] * 4u);
+  const __amdgpu_buffer_rsrc_t rC1 = make_rsrc(a.col_idx + beg[1], (uint32_t)len[1] * 4u);
+  auto load_chunk = [&](int r, int c) -> int {
+    return __builtin_amdgcn_raw_buffer_load_b32(r == 0 ? rC0 : rC1, (uint32_t)(c * 64 + lane) * 4u, 0, 0);
+  };
+  // Validation: every entry in [0, NB) and each row strictly ascending;
+  // whether a row keeps the ragged last block (always its last entry).
+  const bool ragged_L = L % 64 != 0;
+  bool slow = false;
+  int rag = 0;                        // bit r: row r keeps the ragged block
+#pragma unroll
+  for (int r = 0; r < 2; ++r) {
+    int last = -1;
+    for (int c = 0; c * 64 < len[r]; ++c) {
+      const int n = c * 64 + lane;
+      const int v = load_chunk(r, c);
+      int prev = __shfl_up(v, 1, 64);
+      if (lane == 0) prev = last;
+      const bool valid = n < len[r];
+      if (__any(valid && (v < 0 || v >= nkb || v <= prev))) slow = true;
+      if (__any(valid && ragged_L && v == nkb - 1)) rag |= 1 << r;
+      last = __builtin_amdgcn_readlane(v, 63);
+    }
+  }
+  // Size of the union: |A| + |B| - |A and B|, the intersection counted with a
+  // byte map of row A's blocks in V slot 0 (read before that slot's first
+  // load, which follows the prologue's barriers).
+  uint8_t* mark = reinterpret_cast<uint8_t*>(sV[0]);
+  int inter = 0;
+  __syncthreads();                    // slot 0 zeroed by every thread
+  if (!slow) {
+    for (int c = 0; c * 64 < len[0]; ++c) {
+      const int v = load_chunk(0, c);
+      if (c * 64 + lane < len[0]) mark[v] = 1;
+    }
+  }
+  __syncthreads();
+  if (!slow) {
+    for (int c = 0; c * 64 < len[1]; ++c) {
+      const int v = load_chunk(1, c);
+      inter += __builtin_popcountll(__ballot(c * 64 + lane < len[1] && mark[v] == 1));
+    }
+  }
+  // The pipeline walks the union without the ragged block (done masked).
+  const int na = len[0] - (rag & 1), nb = len[1] - ((rag >> 1) & 1);
+  const int nf = slow ? 0 : na + nb - (inter - (rag == 3 ? 1 : 0));
+
+  // Merge state: next unread entry of each row and two-chunk windows.
+  int head[2] = {0, 0}, win[2] = {0, 0};
+  int w0[2], w1[2];
+#pragma unroll
+  for (int r = 0; r < 2; ++r) {
+    w0[r] = load_chunk(r, 0);
+    w1[r] = load_chunk(r, 1);
+  }
+  // Next block of the union (ascending) and which rows keep it; both heads
+  // are read before a window moves (the new chunk is first read 64 entries
+  // later).
+  auto next_union = [&](int& blk, int& keep) {
+    int v[2];
+#pragma unroll
+    for (int r = 0; r < 2; ++r) {
+      const int i = head[r];
+      const int x0 = __builtin_amdgcn_readlane(w0[r], i & 63);
+      const int x1 = __builtin_amdgcn_readlane(w1[r], i & 63);
+      v[r] = i < (r == 0 ? na : nb) ? ((i >> 6) == win[r] ? x0 : x1) : INT_MAX;
+    }
+    blk = v[0] < v[1] ? v[0] : v[1];
+    keep = (v[0] == blk ? 1 : 0) | (v[1] == blk ? 2 : 0);
+#pragma unroll
+    for (int r = 0; r < 2; ++r) {
+      if (keep & (1 << r)) {
+        ++head[r];
+        if ((head[r] >> 6) > win[r]) {
+          w0[r] = w1[r];
+          w1[r] = load_chunk(r, win[r] + 2);
+          ++win[r];
+        }
+      }
+    }
+  };
+
+  const float sl2 = a.scale_log2;
+  const float thr = kRescaleLog2 / sl2;
+  float m = -INFINITY, lsum = 0.f;
+  f32x16 o[ND];
+#pragma unroll
+  for (int d = 0; d < ND; ++d) o[d] = f32x16{};
+  auto hide = [&](f32x16 (&s)[2]) {   // this half does not keep the tile
+#pragma unroll
+    for (int g = 0; g < 2; ++g)
+#pragma unroll
+      for (int e = 0; e < 16; ++e) s[g][e] = -INFINITY;
+  };
+  __syncthreads();                    // block map reads done
+
+  if (nf > 0) {
+    // Union entries t, t+1, t+2 (block, keep bits) for step t.
+    int ub[3] = {0, 0, 0}, uk[3] = {0, 0, 0};
+#pragma unroll
+    for (int j = 0; j < 3; ++j)
+      if (j < nf) next_union(ub[j], uk[j]);
+    KDMA::issue(rK, sK[0], ub[0] * 64, wave, lane);
+    if (nf > 1) KDMA::issue(rK, sK[1], ub[1] * 64, wave, lane);
+    wait_vmem();
+    __syncthreads();
+    f32x16 s_cur[2];
+    qk_tile<D, KS>(sK[0], qf, c32, hw, s_cur);
+    if (!(uk[0] & mybit)) hide(s_cur);
+    __syncthreads();                  // sK[0] is refilled by step 0
+
+    bf16x8 p_prev[2][2];
+#pragma unroll
+    for (int g = 0; g < 2; ++g)
+#pragma unroll
+      for (int s2 = 0; s2 < 2; ++s2) p_prev[g][s2] = bf16x8{};
+    bool pend = false;
+    float pend_alpha = 1.f;
+    KVLoader<D, NW> ld;
+    ld.init(wave, lane);
+
+    // Step t reads K(t+1) and V(t-1) and loads K(t+2) and V(t), as in
+    // attn_fwd_kernel; tile j is union entry j.
+    auto step = [&](int t, const u16* rdK, const u16* rdV, u16* ldK, u16* ldV) {
+      if (pend) {
+#pragma unroll
+        for (int d = 0; d < ND; ++d)
+#pragma unroll
+          for (int e = 0; e < 16; ++e) o[d][e] *= pend_alpha;
+      }
+      const bool kload = t + 2 < nf;
+      uint32_t kbyte = kload ? (uint32_t)ub[2] * (uint32_t)(64 * D * 2) : 0u;
+      uint32_t vbyte = (uint32_t)ub[0] * (uint32_t)(64 * D * 2);
+      asm volatile("" : "+s"(kbyte), "+s"(vbyte));
+      int wv = wave;
+      asm volatile("" : "+s"(wv));
+      auto loads = [&](int slot) {
+        constexpr int PK = KVLoader<D, NW>::PWK, NTOT = PK + KVLoader<D, NW>::PWV;
+        constexpr int NM = 2 * NK + 4 * ND;
+        static_assert(NTOT <= NM, "one load instruction per slot at most");
+        const int n = (slot * NTOT + NM - 1) / NM;
+        if (n >= NTOT || (n * NM) / NTOT != slot) return;
+        if (n < PK) {
+          if (kload) ld.k(rK, ldK, kbyte, n, wv);
+        } else {
+          ld.v(rV, ldV, vbyte, n - PK, wv);
+        }
+      };
+      f32x16 s_next[2];
+      bf16x8 p_cur[2][2];
+      pipelined_step<D, KS, VS>(loads, rdK + klane, rdV + voff, qf, s_cur, p_prev, s_next, p_cur, o, m,
+                                lsum, thr, sl2, pend_alpha, pend);
+#pragma unroll
+      for (int g = 0; g < 2; ++g) {
+        s_cur[g] = s_next[g];
+#pragma unroll
+        for (int s2 = 0; s2 < 2; ++s2) p_prev[g][s2] = p_cur[g][s2];
+      }
+      if (!(uk[1] & mybit)) hide(s_cur);   // scores of tile t+1
+      ub[0] = ub[1];
+      uk[0] = uk[1];
+      ub[1] = ub[2];
+      uk[1] = uk[2];
+      if (t + 3 < nf) next_union(ub[2], uk[2]);
+      wait_vmem();
+      __syncthreads();
+    };
+    int t = 0;
+    for (; t + 1 < nf; t += 2) {
+      step(t, sK[1], sV[1], sK[0], sV[0]);
+      step(t + 1, sK[0], sV[0], sK[1], sV[1]);
+    }
+    if (t < nf) step(t, sK[1], sV[1], sK[0], sV[0]);
+    if (pend) {
+#pragma unroll
+      for (int d = 0; d < ND; ++d)
+#pragma unroll
+        for (int e = 0; e < 16; ++e) o[d][e] *= pend_alpha;
+    }
+    pv_tile<ND, VS>(sV[(nf - 1) & 1] + voff, p_prev, o);
+    __syncthreads();
+  }
+
+  // One tile with key masking, kept by the rows in keep.
+  auto masked_tile = [&](int kb, int keep) {
+    KDMA::issue(rK, sK[0], kb, wave, lane);
+    VDMA::issue(rV, sV[0], kb, wave, lane);
+    wait_vmem();
+    __syncthreads();
+    f32x16 s[2];
+    qk_tile<D, KS>(sK[0], qf, c32, hw, s);
+    mask_tile(s, L - kb, hw);
+    if (!(keep & mybit)) hide(s);
+    bf16x8 pb[2][2];
+    float alpha;
+    bool moved;
+    softmax_tile(s, m, lsum, thr, sl2, pb, alpha, moved);
+    if (moved) {
+#pragma unroll
+      for (int d = 0; d < ND; ++d)
+#pragma unroll
+        for (int e = 0; e < 16; ++e) o[d][e] *= alpha;
+    }
+    pv_tile<ND, VS>(sV[0] + voff, pb, o);
+    __syncthreads();
+  };
+  if (slow) {
+    // Malformed rows: each row's valid entries in its own order.
+#pragma unroll
+    for (int r = 0; r < 2; ++r)
+      for (int i = 0; i < len[r]; ++i) {
+        const int c = a.col_idx[beg[r] + i];
+        if (c >= 0 && c < nkb) masked_tile(c * 64, 1 << r);
+      }
+  } else if (rag) {
+    masked_tile((nkb - 1) * 64, rag);
+  }
+
+  float lt;
+  {
+    float lo, hi;
+    half_pair(lsum, lo, hi);
+    lt = lo + hi;
+  }
+  const float inv = lt > 0.f ? 1.f / lt : 0.f;
+  if (qrow < L) {
+    u16* orow = a.o + hoff + (size_t)qrow * D;
+#pragma unroll
+    for (int d = 0; d < ND; ++d)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        bf16x4 w;
+#pragma unroll
+        for (int j = 0; j < 4; ++j) w[j] = (__bf16)(o[d][4 * i + j] * inv);
+        *reinterpret_cast<bf16x4*>(orow + d * 32 + 8 * i + 4 * hw) = w;
+      }
+    if (hw == 0 && a.lse != nullptr)
+      a.lse[(size_t)bh * L + qrow] = lt > 0.f ? fmaf(m, a.scale, logf(lt)) : -INFINITY;
+  }
+}
+
+// ---------------------------------------------------------------------------
 // Block attention mass: W[p][c] = sum_{i in p, j in c} exp(scale*q_i.k_j - LSE_i)
 //
 // One workgroup of four waves (32 rows each) covers 128 query rows: one query
@@ -490,13 +805,22 @@ hipError_t launch_dense(AttnParams a, int D, hipStream_t st) {
 }
 
 hipError_t launch_sparse(AttnParams a, int D, hipStream_t st) {
-  // One workgroup per query block (block / 32 waves).
+  if (a.block == 64) {
+    // One workgroup per pair of query blocks (128 rows); text ranges in pairs.
+    a.nqt = (a.nkb + 1) / 2;
+    a.n_wg = a.nqt * a.batch_heads;
+    if (a.tq1 > a.tq0) {
+      a.tq0 = a.tq0 / 2;
+      a.tq1 = (a.tq1 + 1) / 2;
+      if (a.tq1 - a.tq0 >= a.nqt) a.tq0 = a.tq1 = 0;
+    }
+    if (D == 64) hipLaunchKernelGGL(attn_sparse_pair_kernel<64>, dim3(a.n_wg), dim3(256), 0, st, a);
+    else hipLaunchKernelGGL(attn_sparse_pair_kernel<128>, dim3(a.n_wg), dim3(256), 0, st, a);
+    return hipGetLastError();
+  }
+  // One workgroup per query block of 128 (four waves).
   a.nqt = a.nkb;
   a.n_wg = a.nkb * a.batch_heads;
-  if (a.block == 64) {
-    if (D == 64) return launch_attn<64, 2, true>(a, st);
-    return launch_attn<128, 2, true>(a, st);
-  }
   if (D == 64) return launch_attn<64, 4, true>(a, st);
   return launch_attn<128, 4, true>(a, st);
 }
