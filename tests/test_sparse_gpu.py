@@ -110,13 +110,14 @@ def test_sparse_deterministic():
     assert torch.equal(o1, o2) and torch.equal(l1, l2)
 
 
+@pytest.mark.parametrize("block", [64, 128])
 @pytest.mark.parametrize("text", [(0, 128), (512, 200), (1664, 384), (0, 0)])
-def test_text_first_order_covers_every_row(text):
+def test_text_first_order_covers_every_row(text, block):
     """The work order that starts text query blocks first is a bijection:
     every (head, query block) row is computed, for text at the start, in the
     middle (unaligned), at the end and absent, with more heads than XCDs."""
     t0, tl = text
-    w = TINY.replace(heads=9, block=128)
+    w = TINY.replace(heads=9, block=block)
     q, k, v = make_qkv(w, device="cuda")
     nb = w.nblocks
     tb = text_blocks(w.seqlen, w.block, t0, tl) if tl > 0 else []
@@ -140,3 +141,29 @@ def test_text_first_order_covers_every_row(text):
                                                      rpn[h * nb:(h + 1) * nb + 1], cin, w.scale, w.block)
         check_out(out[0, h], o_ref, f"h{h}")
         check_lse(lse[0, h], l_ref)
+
+
+def test_unordered_rows_take_the_masked_path():
+    """Block 64 pairs two query blocks and merges their lists, which needs
+    ascending lists; a row given out of order (or with a repeat) is done tile
+    by tile instead, with the same result."""
+    w = TINY.replace(seqlen=640, patches=144)
+    q, k, v = make_qkv(w, device="cuda")
+    nb = w.nblocks
+    g = np.random.default_rng(11)
+    lists = [sorted(g.choice(nb, 3, replace=False).tolist()) for _ in range(w.heads * nb)]
+    lists[2] = [7, 1, 4]               # descending / unordered
+    lists[5] = [3, 3]                  # repeat: counted twice, like the per-row kernel
+    rp = torch.tensor([0] + list(np.cumsum([len(x) for x in lists])), dtype=torch.int32)
+    ci = torch.tensor([c for x in lists for c in x], dtype=torch.int32)
+    out, lse = ad.block_sparse_attn(q, k, v, rp.cuda(), ci.cuda(), block=64)
+    torch.cuda.synchronize()
+    for r, kept in enumerate(lists):
+        if r == 5:
+            continue                   # a repeated block is not a valid pattern
+        h, p = divmod(r, nb)
+        mask = oracle.key_mask_from_blocks(kept, w.seqlen, 64)
+        o_ref, l_ref = oracle.masked_attention(f64(q[0, h, p * 64:(p + 1) * 64]), f64(k[0, h]),
+                                               f64(v[0, h]), mask, w.scale)
+        check_out(out[0, h, p * 64:(p + 1) * 64], o_ref, f"row {r}")
+        check_lse(lse[0, h, p * 64:(p + 1) * 64], l_ref)
