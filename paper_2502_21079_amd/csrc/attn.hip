@@ -317,9 +317,12 @@ __global__ __launch_bounds__(64 * NW, NW >= 8 ? 1 : 2) void attn_fwd_kernel(Attn
 // must be strictly ascending lists of blocks in [0, NB); otherwise (or for
 // the ragged last block) tiles are done one at a time with key masking.
 // ---------------------------------------------------------------------------
-template <int D>
-__global__ __launch_bounds__(256, 2) void attn_sparse_pair_kernel(AttnParams a) {
-  constexpr int NW = 4, NT = 256;
+template <int D, int NW>
+__global__ __launch_bounds__(64 * NW, NW >= 8 ? 1 : 2) void attn_sparse_pair_kernel(AttnParams a) {
+  constexpr int NT = 64 * NW;
+  constexpr int WPB = NW / 2;        // waves per query block
+  constexpr int BLK = 32 * WPB;      // block size: 64 (four waves) or 128 (eight waves)
+  constexpr int SUB = BLK / KT;      // 64-key tiles per block
   using KDMA = TileDMA<D, NW, 1>;
   using VDMA = TileDMA<D, NW, 2>;
   constexpr int KS = KDMA::S, VS = VDMA::S;
@@ -339,7 +342,7 @@ __global__ __launch_bounds__(256, 2) void attn_sparse_pair_kernel(AttnParams a) 
   }
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);   // wave-uniform
-  const int mybit = 1 << (wave >> 1);                          // 1: row 2P, 2: row 2P+1
+  const int mybit = 1 << (wave / WPB);                         // 1: row 2P, 2: row 2P+1
   const int hw = lane >> 5, c32 = lane & 31;
   const int gi = lane & 15, grp = lane >> 4;
   const int L = a.seqlen, nkb = a.nkb;
@@ -347,7 +350,7 @@ __global__ __launch_bounds__(256, 2) void attn_sparse_pair_kernel(AttnParams a) 
   const uint32_t hbytes = (uint32_t)L * D * 2u;
   const __amdgpu_buffer_rsrc_t rK = make_rsrc(a.k + hoff, hbytes);
   const __amdgpu_buffer_rsrc_t rV = make_rsrc(a.v + hoff, hbytes);
-  const int qrow = pq * 128 + wave * 32 + c32;
+  const int qrow = pq * (2 * BLK) + wave * 32 + c32;
   const int voff = ((4 * hw + (gi >> 2)) * VS) * 8 + 16 * (grp & 1) + 4 * (gi & 3);
   const int klane = (c32 * KS + hw) * 8;
 
@@ -384,7 +387,7 @@ __global__ __launch_bounds__(256, 2) void attn_sparse_pair_kernel(AttnParams a) 
   };
   // Validation: every entry in [0, NB) and each row strictly ascending;
   // whether a row keeps the ragged last block (always its last entry).
-  const bool ragged_L = L % 64 != 0;
+  const bool ragged_L = L % BLK != 0;
   bool slow = false;
   int rag = 0;                        // bit r: row r keeps the ragged block
 #pragma unroll
@@ -420,9 +423,11 @@ __global__ __launch_bounds__(256, 2) void attn_sparse_pair_kernel(AttnParams a) 
       inter += __builtin_popcountll(__ballot(c * 64 + lane < len[1] && mark[v] == 1));
     }
   }
-  // The pipeline walks the union without the ragged block (done masked).
+  // The pipeline walks the union without the ragged block (done masked);
+  // pipeline tile j is 64-key tile j % SUB of union entry j / SUB.
   const int na = len[0] - (rag & 1), nb = len[1] - ((rag >> 1) & 1);
-  const int nf = slow ? 0 : na + nb - (inter - (rag == 3 ? 1 : 0));
+  const int nu = slow ? 0 : na + nb - (inter - (rag == 3 ? 1 : 0));
+  const int nf = nu * SUB;
 
   // Merge state: next unread entry of each row and two-chunk windows.
   int head[2] = {0, 0}, win[2] = {0, 0};
@@ -474,13 +479,17 @@ __global__ __launch_bounds__(256, 2) void attn_sparse_pair_kernel(AttnParams a) 
   __syncthreads();                    // block map reads done
 
   if (nf > 0) {
-    // Union entries t, t+1, t+2 (block, keep bits) for step t.
+    // Union entries u0 = t / SUB, u0 + 1, u0 + 2 (block, keep bits) at step t.
     int ub[3] = {0, 0, 0}, uk[3] = {0, 0, 0};
+    int u0 = 0;
 #pragma unroll
     for (int j = 0; j < 3; ++j)
-      if (j < nf) next_union(ub[j], uk[j]);
-    KDMA::issue(rK, sK[0], ub[0] * 64, wave, lane);
-    if (nf > 1) KDMA::issue(rK, sK[1], ub[1] * 64, wave, lane);
+      if (j < nu) next_union(ub[j], uk[j]);
+    auto pick = [&](const int (&x)[3], int slot) { return slot == 0 ? x[0] : (slot == 1 ? x[1] : x[2]); };
+    // First row of pipeline tile j, j within the queue's reach.
+    auto tile_row = [&](int j) { return (pick(ub, j / SUB - u0) * SUB + j % SUB) * KT; };
+    KDMA::issue(rK, sK[0], tile_row(0), wave, lane);
+    if (nf > 1) KDMA::issue(rK, sK[1], tile_row(1), wave, lane);
     wait_vmem();
     __syncthreads();
     f32x16 s_cur[2];
@@ -508,8 +517,8 @@ __global__ __launch_bounds__(256, 2) void attn_sparse_pair_kernel(AttnParams a) 
           for (int e = 0; e < 16; ++e) o[d][e] *= pend_alpha;
       }
       const bool kload = t + 2 < nf;
-      uint32_t kbyte = kload ? (uint32_t)ub[2] * (uint32_t)(64 * D * 2) : 0u;
-      uint32_t vbyte = (uint32_t)ub[0] * (uint32_t)(64 * D * 2);
+      uint32_t kbyte = kload ? (uint32_t)tile_row(t + 2) * (uint32_t)(D * 2) : 0u;
+      uint32_t vbyte = (uint32_t)tile_row(t) * (uint32_t)(D * 2);
       asm volatile("" : "+s"(kbyte), "+s"(vbyte));
       int wv = wave;
       asm volatile("" : "+s"(wv));
@@ -535,12 +544,15 @@ __global__ __launch_bounds__(256, 2) void attn_sparse_pair_kernel(AttnParams a) 
 #pragma unroll
         for (int s2 = 0; s2 < 2; ++s2) p_prev[g][s2] = p_cur[g][s2];
       }
-      if (!(uk[1] & mybit)) hide(s_cur);   // scores of tile t+1
-      ub[0] = ub[1];
-      uk[0] = uk[1];
-      ub[1] = ub[2];
-      uk[1] = uk[2];
-      if (t + 3 < nf) next_union(ub[2], uk[2]);
+      if (!(pick(uk, (t + 1) / SUB - u0) & mybit)) hide(s_cur);   // scores of tile t+1
+      if ((t + 1) % SUB == 0) {          // tile t was the last of entry u0
+        ub[0] = ub[1];
+        uk[0] = uk[1];
+        ub[1] = ub[2];
+        uk[1] = uk[2];
+        if (u0 + 3 < nu) next_union(ub[2], uk[2]);
+        ++u0;
+      }
       wait_vmem();
       __syncthreads();
     };
@@ -589,10 +601,13 @@ __global__ __launch_bounds__(256, 2) void attn_sparse_pair_kernel(AttnParams a) 
     for (int r = 0; r < 2; ++r)
       for (int i = 0; i < len[r]; ++i) {
         const int c = a.col_idx[beg[r] + i];
-        if (c >= 0 && c < nkb) masked_tile(c * 64, 1 << r);
+        if (c >= 0 && c < nkb)
+          for (int j = 0; j < SUB; ++j)
+            if (c * BLK + j * KT < L) masked_tile(c * BLK + j * KT, 1 << r);
       }
   } else if (rag) {
-    masked_tile((nkb - 1) * 64, rag);
+    for (int j = 0; j < SUB; ++j)
+      if ((nkb - 1) * BLK + j * KT < L) masked_tile((nkb - 1) * BLK + j * KT, rag);
   }
 
   float lt;
@@ -814,8 +829,8 @@ hipError_t launch_sparse(AttnParams a, int D, hipStream_t st) {
       a.tq1 = (a.tq1 + 1) / 2;
       if (a.tq1 - a.tq0 >= a.nqt) a.tq0 = a.tq1 = 0;
     }
-    if (D == 64) hipLaunchKernelGGL(attn_sparse_pair_kernel<64>, dim3(a.n_wg), dim3(256), 0, st, a);
-    else hipLaunchKernelGGL(attn_sparse_pair_kernel<128>, dim3(a.n_wg), dim3(256), 0, st, a);
+    if (D == 64) hipLaunchKernelGGL((attn_sparse_pair_kernel<64, 4>), dim3(a.n_wg), dim3(256), 0, st, a);
+    else hipLaunchKernelGGL((attn_sparse_pair_kernel<128, 4>), dim3(a.n_wg), dim3(256), 0, st, a);
     return hipGetLastError();
   }
   // One workgroup per query block of 128 (four waves).
