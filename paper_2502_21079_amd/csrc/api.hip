@@ -119,9 +119,12 @@ namespace adaspa {
 // Work-to-XCD mapping (see the kernels): 1 gives each XCD one contiguous range
 // of (head, query tile) work items, so the workgroups sharing an L2 stream the
 // same K/V (dense attention and the mass pass: about 6x less HBM traffic than
-// hardware order; block-sparse attention: neighbouring query blocks select
-// largely the same key blocks); 0 keeps the hardware's round-robin order; 2 is
-// the head-chunked order.  ADASPA_XCD_MAP overrides the per-kernel choice.
+// hardware order); 0 keeps the hardware's round-robin order; 2 is the
+// head-chunked order; 3 (block-sparse attention) starts the text query blocks
+// first and then gives each XCD an equal contiguous share of every head, so
+// heads of different density stay balanced and neighbouring query blocks,
+// which select largely the same key blocks, share an L2.  ADASPA_XCD_MAP
+// overrides the per-kernel choice.
 int xcd_map_mode(int kernel_default) {
   static const int env = [] {
     const char* e = getenv("ADASPA_XCD_MAP");
@@ -302,7 +305,7 @@ adaspa_status adaspa_block_sparse_attn(const adaspa_problem* prob, const void* q
   a.nkb = num_blocks(prob);
   a.scale = scale_of(prob);
   a.scale_log2 = a.scale * 1.4426950408889634f;
-  a.xcd_map = xcd_map_mode(1);
+  a.xcd_map = xcd_map_mode(3);
   // Text query blocks keep every key block under the text sink, so they are
   // the longest rows; the kernel starts them first (the result does not
   // depend on the order).

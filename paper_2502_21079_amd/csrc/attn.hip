@@ -40,8 +40,8 @@ __global__ __launch_bounds__(64 * NW, NW >= 8 ? 1 : 2) void attn_fwd_kernel(Attn
   int bh, qt;
   if (a.xcd_map == 2) {
     xcd_chunk_map(blockIdx.x, a.nqt, a.batch_heads, bh, qt);
-  } else if (SPARSE && a.xcd_map == 1 && a.tq1 > a.tq0) {
-    text_first_map(blockIdx.x, a.n_wg, a.nqt, a.tq0, a.tq1 - a.tq0, bh, qt);
+  } else if (SPARSE && (a.xcd_map == 1 || a.xcd_map == 3)) {
+    text_first_map(blockIdx.x, a.n_wg, a.nqt, a.tq0, a.tq1 - a.tq0, bh, qt, a.xcd_map == 3);
   } else {
     const int lid = a.xcd_map ? xcd_remap(blockIdx.x, a.n_wg) : (int)blockIdx.x;
     bh = lid / a.nqt;
@@ -333,8 +333,8 @@ __global__ __launch_bounds__(64 * NW, NW >= 8 ? 1 : 2) void attn_sparse_pair_ker
   __shared__ __attribute__((aligned(1024))) u16 sV[2][VDMA::ELEMS];
 
   int bh, pq;
-  if (a.xcd_map == 1 && a.tq1 > a.tq0) {
-    text_first_map(blockIdx.x, a.n_wg, a.nqt, a.tq0, a.tq1 - a.tq0, bh, pq);
+  if (a.xcd_map == 1 || a.xcd_map == 3) {
+    text_first_map(blockIdx.x, a.n_wg, a.nqt, a.tq0, a.tq1 - a.tq0, bh, pq, a.xcd_map == 3);
   } else {
     const int lid = a.xcd_map ? xcd_remap(blockIdx.x, a.n_wg) : (int)blockIdx.x;
     bh = lid / a.nqt;

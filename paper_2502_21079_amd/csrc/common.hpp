@@ -93,9 +93,14 @@ __device__ __forceinline__ float dpp_plus(float v) {
 // xcd_remap.  In block-sparse attention the text query blocks keep every key
 // block, so they are the longest rows by far; starting them first removes the
 // tail they would otherwise leave.  Bijective for any sizes.
+// With chunked, the other tiles follow in (chunk, head, tile) order instead,
+// chunk c holding tiles [c*m/8, (c+1)*m/8) of every head (m tiles per head),
+// so each XCD also receives an equal share of every head (heads of different
+// cost stay balanced) in contiguous runs.
 __device__ __forceinline__ void text_first_map(int hid, int n, int nqt, int tq0, int ntq, int& bh,
-                                               int& qt) {
-  const int nt = ntq * (n / nqt);
+                                               int& qt, bool chunked = false) {
+  const int nbh = n / nqt;
+  const int nt = ntq * nbh;
   if (hid < nt) {
     bh = hid / ntq;
     qt = tq0 + hid % ntq;
@@ -106,8 +111,21 @@ __device__ __forceinline__ void text_first_map(int hid, int n, int nqt, int tq0,
   int lid = cnt(hid, x) - cnt(nt, x);
   for (int y = 0; y < x; ++y) lid += cnt(n, y) - cnt(nt, y);
   const int nvq = nqt - ntq;
-  bh = lid / nvq;
-  const int r = lid % nvq;
+  int r;
+  if (!chunked) {
+    bh = lid / nvq;
+    r = lid % nvq;
+  } else {
+    int c = 0, start = 0;
+    for (; c < 7; ++c) {
+      const int sz = ((c + 1) * nvq) / 8 - (c * nvq) / 8;
+      if (lid < start + sz * nbh) break;
+      start += sz * nbh;
+    }
+    const int c0 = (c * nvq) / 8, sz = ((c + 1) * nvq) / 8 - c0;
+    bh = (lid - start) / sz;
+    r = c0 + (lid - start) % sz;
+  }
   qt = r < tq0 ? r : r + ntq;
 }
 

@@ -25,7 +25,8 @@ struct AttnParams {
   int n_wg;                   // workgroups (set by the launcher)
   float scale;
   float scale_log2;           // scale * log2(e)
-  int xcd_map;                // 0 hardware order, 1 contiguous per XCD, 2 head-chunked
+  int xcd_map;                // 0 hardware order, 1 contiguous per XCD, 2 head-chunked,
+                              // 3 sparse: text first, then head-chunked
   int tq0, tq1;               // sparse: text query blocks [tq0, tq1), dispatched first
 };
 
