@@ -60,12 +60,11 @@ __global__ __launch_bounds__(64 * NW, NW >= 8 ? 1 : 2) void attn_fwd_kernel(Attn
   const int voff = ((4 * hw + (gi >> 2)) * VS) * 8 + 16 * (grp & 1) + 4 * (gi & 3);
   const int klane = (c32 * KS + hw) * 8;
 
-  // Finite contents everywhere, whatever a bounds-checked load leaves behind.
+  // V slots hold finite values whatever a bounds-checked load leaves behind
+  // (a key masked to -inf still multiplies its V row by a zero probability);
+  // K rows past the sequence are masked whatever they hold.
 #pragma unroll
-  for (int b = 0; b < RING; ++b) {
-    zero_lds<VDMA::SLOTS>(sV[b], tid, NT);
-    zero_lds<KDMA::SLOTS>(sK[b], tid, NT);
-  }
+  for (int b = 0; b < RING; ++b) zero_lds<VDMA::SLOTS>(sV[b], tid, NT);
 
   bf16x8 qf[NK];
   load_q<D>(a.q + hoff, qrow, L, hw, qf);
@@ -97,18 +96,20 @@ __global__ __launch_bounds__(64 * NW, NW >= 8 ? 1 : 2) void attn_fwd_kernel(Attn
     e0 = (int)s;
     ne = (int)(e - s);
     rC = make_rsrc(a.col_idx + e0, (uint32_t)ne * 4u);
+    // The first two chunks are the window's; the validation scan reads them
+    // from there (one memory round trip less before the first tile loads).
+    cid0 = load_chunk(0);
+    cid1 = load_chunk(1);
     const bool ragged = L % a.block != 0;
     for (int c = 0; c * 64 < ne; ++c) {
       const int n = c * 64 + lane;
-      const int v = load_chunk(c);
+      const int v = c == 0 ? cid0 : (c == 1 ? cid1 : load_chunk(c));
       if (__any(n < ne && (v < 0 || v >= a.nkb))) slow = true;
       const unsigned long long rb = __ballot(n < ne && ragged && v == a.nkb - 1);
       if (skip < 0 && rb != 0ull) skip = c * 64 + __builtin_ctzll(rb);
     }
     nf = slow ? 0 : (ne - (skip >= 0 ? 1 : 0)) * SUB;
     skip_at = skip >= 0 ? skip : INT_MAX;
-    cid0 = load_chunk(0);
-    cid1 = load_chunk(1);
   } else {
     nf = L / KT;
   }
@@ -355,10 +356,7 @@ __global__ __launch_bounds__(64 * NW, NW >= 8 ? 1 : 2) void attn_sparse_pair_ker
   const int klane = (c32 * KS + hw) * 8;
 
 #pragma unroll
-  for (int b = 0; b < 2; ++b) {
-    zero_lds<VDMA::SLOTS>(sV[b], tid, NT);
-    zero_lds<KDMA::SLOTS>(sK[b], tid, NT);
-  }
+  for (int b = 0; b < 2; ++b) zero_lds<VDMA::SLOTS>(sV[b], tid, NT);   // finite V; the block map
   bf16x8 qf[NK];
   load_q<D>(a.q + hoff, qrow, L, hw, qf);
 
@@ -385,6 +383,15 @@ __global__ __launch_bounds__(64 * NW, NW >= 8 ? 1 : 2) void attn_sparse_pair_ker
   auto load_chunk = [&](int r, int c) -> int {
     return __builtin_amdgcn_raw_buffer_load_b32(r == 0 ? rC0 : rC1, (uint32_t)(c * 64 + lane) * 4u, 0, 0);
   };
+  // Two-chunk windows of each row, loaded first; the prologue's scans read
+  // chunks 0 and 1 from them.
+  int w0[2], w1[2];
+#pragma unroll
+  for (int r = 0; r < 2; ++r) {
+    w0[r] = load_chunk(r, 0);
+    w1[r] = load_chunk(r, 1);
+  }
+  auto chunk = [&](int r, int c) -> int { return c == 0 ? w0[r] : (c == 1 ? w1[r] : load_chunk(r, c)); };
   // Validation: every entry in [0, NB) and each row strictly ascending;
   // whether a row keeps the ragged last block (always its last entry).
   const bool ragged_L = L % BLK != 0;
@@ -395,7 +402,7 @@ __global__ __launch_bounds__(64 * NW, NW >= 8 ? 1 : 2) void attn_sparse_pair_ker
     int last = -1;
     for (int c = 0; c * 64 < len[r]; ++c) {
       const int n = c * 64 + lane;
-      const int v = load_chunk(r, c);
+      const int v = chunk(r, c);
       int prev = __shfl_up(v, 1, 64);
       if (lane == 0) prev = last;
       const bool valid = n < len[r];
@@ -412,14 +419,14 @@ __global__ __launch_bounds__(64 * NW, NW >= 8 ? 1 : 2) void attn_sparse_pair_ker
   __syncthreads();                    // slot 0 zeroed by every thread
   if (!slow) {
     for (int c = 0; c * 64 < len[0]; ++c) {
-      const int v = load_chunk(0, c);
+      const int v = chunk(0, c);
       if (c * 64 + lane < len[0]) mark[v] = 1;
     }
   }
   __syncthreads();
   if (!slow) {
     for (int c = 0; c * 64 < len[1]; ++c) {
-      const int v = load_chunk(1, c);
+      const int v = chunk(1, c);
       inter += __builtin_popcountll(__ballot(c * 64 + lane < len[1] && mark[v] == 1));
     }
   }
@@ -429,14 +436,8 @@ __global__ __launch_bounds__(64 * NW, NW >= 8 ? 1 : 2) void attn_sparse_pair_ker
   const int nu = slow ? 0 : na + nb - (inter - (rag == 3 ? 1 : 0));
   const int nf = nu * SUB;
 
-  // Merge state: next unread entry of each row and two-chunk windows.
+  // Merge state: next unread entry of each row (windows w0/w1 above).
   int head[2] = {0, 0}, win[2] = {0, 0};
-  int w0[2], w1[2];
-#pragma unroll
-  for (int r = 0; r < 2; ++r) {
-    w0[r] = load_chunk(r, 0);
-    w1[r] = load_chunk(r, 1);
-  }
   // Next block of the union (ascending) and which rows keep it; both heads
   // are read before a window moves (the new chunk is first read 64 entries
   // later).
@@ -678,8 +679,6 @@ __global__ __launch_bounds__(256, 2) void block_mass_kernel(MassParams a) {
   const int qrow = pg * 128 + wave * 32 + c32;
   const bool qvalid = qrow < L;
 
-  zero_lds<KDMA::SLOTS>(sK0, tid, NT);
-  zero_lds<KDMA::SLOTS>(sK1, tid, NT);
   bf16x8 qf[NK];
   load_q<D>(a.q + hoff, qrow, L, hw, qf);
   const float sl2 = a.scale_log2;
