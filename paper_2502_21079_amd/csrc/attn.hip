@@ -29,13 +29,15 @@ __global__ __launch_bounds__(64 * NW, NW >= 8 ? 1 : 2) void attn_fwd_kernel(Attn
   constexpr int KS = KDMA::S, VS = VDMA::S;
   constexpr int ND = D / 32;   // 32-wide output column blocks
   constexpr int NK = D / 16;   // MFMA k-steps over the head dimension
-  // K and V rings of RING tiles.  Tiles are loaded HALF = RING/2 steps before
-  // the step that reads them and the waves meet at a barrier every HALF steps.
-  // Two tiles (a barrier every step) measured faster than four tiles (a
-  // barrier every second step) for the dense kernel on gfx950.
-  constexpr int RING = 2, HALF = RING / 2;
-  __shared__ __attribute__((aligned(1024))) u16 sK[RING][KDMA::ELEMS];
-  __shared__ __attribute__((aligned(1024))) u16 sV[RING][VDMA::ELEMS];
+  // A ring of two slots, each [K tile | V tile]; step t reads K(t+1) and
+  // V(t-1) from one slot while K(t+2) and V(t) are loaded into the other,
+  // and the waves meet at a barrier every step.  (Two slots measured faster
+  // than four with a barrier every second step for the dense kernel.)
+  using LD = KVLoader<D, NW>;
+  constexpr int RING = 2;
+  __shared__ __attribute__((aligned(1024))) u16 sKV[RING][LD::ELEMS];   // slots [K | V]
+  const SlotPart<LD::ELEMS, 0> sK{sKV};
+  const SlotPart<LD::ELEMS, LD::VOFF> sV{sKV};
 
   int bh, qt;
   if (a.xcd_map == 2) {
@@ -56,6 +58,7 @@ __global__ __launch_bounds__(64 * NW, NW >= 8 ? 1 : 2) void attn_fwd_kernel(Attn
   const uint32_t hbytes = (uint32_t)L * D * 2u;
   const __amdgpu_buffer_rsrc_t rK = make_rsrc(a.k + hoff, hbytes);
   const __amdgpu_buffer_rsrc_t rV = make_rsrc(a.v + hoff, hbytes);
+  const u32x4 rKw = rsrc_words(a.k + hoff, hbytes), rVw = rsrc_words(a.v + hoff, hbytes);
   const int qrow = qt * (32 * NW) + wave * 32 + c32;
   const int voff = ((4 * hw + (gi >> 2)) * VS) * 8 + 16 * (grp & 1) + 4 * (gi & 3);
   const int klane = (c32 * KS + hw) * 8;
@@ -129,27 +132,23 @@ __global__ __launch_bounds__(64 * NW, NW >= 8 ? 1 : 2) void attn_fwd_kernel(Attn
   };
 
   const float sl2 = a.scale_log2;
-  const float thr = kRescaleLog2 / sl2;   // raw-score margin before the max moves
-  float m = -INFINITY, lsum = 0.f;        // lsum: this lane's half of the row sum
+  RowRef ref;                             // softmax reference of this lane's row
+  float lsum = 0.f;                       // this lane's half of the row sum
   f32x16 o[ND];
 #pragma unroll
   for (int d = 0; d < ND; ++d) o[d] = f32x16{};
   __syncthreads();
 
   if (nf > 0) {
-    // Step t reads K(t+1) and V(t-1), so the first steps need K(0..HALF)
-    // and V(0..HALF-2) in place.
-#pragma unroll
-    for (int j = 0; j <= HALF; ++j)
-      if (j < nf) KDMA::issue(rK, sK[j], kbase(j), wave, lane);
-#pragma unroll
-    for (int j = 0; j <= HALF - 2; ++j)
-      if (j < nf) VDMA::issue(rV, sV[j], kbase(j), wave, lane);
+    // Step t reads K(t+1) and V(t-1), so the first steps need K(0) and K(1)
+    // in place.
+    KDMA::issue(rK, sK[0], kbase(0), wave, lane);
+    if (nf > 1) KDMA::issue(rK, sK[1], kbase(1), wave, lane);
     wait_vmem();
     __syncthreads();
     f32x16 s_cur[2];
     qk_tile<D, KS>(sK[0], qf, c32, hw, s_cur);
-    __syncthreads();            // sK[0] is refilled by step HALF - 1
+    __syncthreads();            // slot 0 is refilled by step 0
 
     bf16x8 p_prev[2][2];
 #pragma unroll
@@ -159,29 +158,30 @@ __global__ __launch_bounds__(64 * NW, NW >= 8 ? 1 : 2) void attn_fwd_kernel(Attn
     bool pend = false;
     float pend_alpha = 1.f;
 
-    KVLoader<D, NW> ld;
+    LD ld;
     ld.init(wave, lane);
+    const u32x4 rMw = ld.mixed_v ? rVw : rKw;     // resource of this wave's mixed entry
 
-    // Step t reads K(t+1) and V(t-1) and loads K(t+1+HALF) and V(t-1+HALF)
-    // into the ring slots read HALF steps earlier (tile j lives in slot
-    // j % RING).  A slot is refilled only after the barrier that follows the
-    // step which read it, and a loaded tile is read only after the barrier
-    // that follows its loads.  The loads are spread over the MFMA slots of
-    // the step: this wave's K instructions first, then its V instructions.
+    // Step t reads K(t+1) and V(t-1) from slot (t+1)&1 and loads K(t+2) and
+    // V(t) into slot t&1, which step t-1 read: a slot is refilled only after
+    // the barrier that follows the step which read it, and a loaded tile is
+    // read only after the barrier that follows its loads.  The loads are
+    // spread over the MFMA slots of the step.  Past the last tile the K
+    // index is clamped to the last one (an in-range load into a slot that is
+    // not read again), so no load depends on a branch.
     auto step = [&](int t, auto sync) {
-      const u16* rdK = sK[(t + 1) & (RING - 1)];
-      const u16* rdV = sV[(t - 1) & (RING - 1)];
-      u16* ldK = sK[(t + 1 + HALF) & (RING - 1)];
-      u16* ldV = sV[(t - 1 + HALF) & (RING - 1)];
-      if (pend) {
+      const int rs = (t + 1) & 1;
+      const u16* rdK = sK[rs];
+      const u16* rdV = sV[rs];
+      if (pend) {             // the reference moved at the previous step
 #pragma unroll
         for (int d = 0; d < ND; ++d)
 #pragma unroll
           for (int e = 0; e < 16; ++e) o[d][e] *= pend_alpha;
+        pend = false;
       }
-      const bool kload = t + 1 + HALF < nf, vload = t - 1 + HALF < nf;
-      uint32_t kbyte = kload ? (uint32_t)kbase(t + 1 + HALF) * (uint32_t)(D * 2) : 0u;
-      uint32_t vbyte = vload ? (uint32_t)kbase(t - 1 + HALF) * (uint32_t)(D * 2) : 0u;
+      uint32_t kbyte = (uint32_t)kbase(t + 2 < nf ? t + 2 : nf - 1) * (uint32_t)(D * 2);
+      uint32_t vbyte = (uint32_t)kbase(t) * (uint32_t)(D * 2);
       if constexpr (SPARSE) {
         // Both entries are read before the window moves, so no read waits
         // for the chunk load below.  Entries advance by at most two per step
@@ -195,28 +195,32 @@ __global__ __launch_bounds__(64 * NW, NW >= 8 ? 1 : 2) void attn_fwd_kernel(Attn
           ++c0;
         }
       }
-      // Re-derived every step: stops the compiler from hoisting one LDS
-      // destination register per load instruction out of the loop (which
-      // overflows the scalar registers); each issue then costs one add.
-      int wv = wave;
-      asm volatile("" : "+s"(wv));
+      // LDS address of the slot being filled, re-derived every step: stops
+      // the compiler from keeping one destination register per load across
+      // the loop (which overflows the scalar registers).
+      uint32_t fill = lds_addr(sKV[t & 1]);
+      asm volatile("" : "+s"(fill));
+      const uint32_t mbyte = ld.mixed_v ? vbyte : kbyte;
       auto loads = [&](int slot) {
-        // Instruction n goes to slot n * NM / NTOT (at most one per slot).
-        constexpr int PK = KVLoader<D, NW>::PWK, NTOT = PK + KVLoader<D, NW>::PWV;
-        constexpr int NM = 2 * NK + 4 * ND;
-        static_assert(NTOT <= NM, "one load instruction per slot at most");
-        const int n = (slot * NTOT + NM - 1) / NM;
-        if (n >= NTOT || (n * NM) / NTOT != slot) return;
-        if (n < PK) {
-          if (kload) ld.k(rK, ldK, kbyte, n, wv);
-        } else {
-          if (vload) ld.v(rV, ldV, vbyte, n - PK, wv);
-        }
+        // Load n goes to slot n * NM / PW (at most one per slot).
+        constexpr int PW = LD::PW, NM = 2 * NK + 4 * ND;
+        static_assert(PW <= NM, "one load instruction per slot at most");
+        const int n = (slot * PW + NM - 1) / NM;
+        if (n >= PW || (n * NM) / PW != slot) return;
+        ld.issue_n(n, fill, rKw, rVw, rMw, kbyte, vbyte, mbyte);
       };
       f32x16 s_next[2];
       bf16x8 p_cur[2][2];
-      pipelined_step<D, KS, VS>(loads, rdK + klane, rdV + voff, qf, s_cur, p_prev, s_next, p_cur, o, m,
-                                lsum, thr, sl2, pend_alpha, pend);
+      float ts;
+      pipelined_step<D, KS, VS>(loads, rdK + klane, rdV + voff, qf, s_cur, p_prev, s_next, p_cur, o, sl2,
+                                ref.mc, ts);
+      if (__any(ts > ref.lim)) {          // rare: the reference moves for this tile
+        pend_alpha = ref.raise(s_cur, sl2);
+        pend = true;
+        lsum *= pend_alpha;
+        ts = exp_tile(s_cur, sl2, ref.mc, p_cur);
+      }
+      lsum += ts;
 #pragma unroll
       for (int g = 0; g < 2; ++g) {
         s_cur[g] = s_next[g];
@@ -230,7 +234,7 @@ __global__ __launch_bounds__(64 * NW, NW >= 8 ? 1 : 2) void attn_fwd_kernel(Attn
     };
     int t = 0;
     for (; t + 1 < nf; t += 2) {
-      step(t, std::integral_constant<bool, HALF == 1>{});
+      step(t, std::true_type{});
       step(t + 1, std::true_type{});
     }
     if (t < nf) step(t, std::true_type{});
@@ -254,15 +258,11 @@ __global__ __launch_bounds__(64 * NW, NW >= 8 ? 1 : 2) void attn_fwd_kernel(Attn
     qk_tile<D, KS>(sK[0], qf, c32, hw, s);
     mask_tile(s, L - kb, hw);
     bf16x8 pb[2][2];
-    float alpha;
-    bool moved;
-    softmax_tile(s, m, lsum, thr, sl2, pb, alpha, moved);
-    if (moved) {
+    const float alpha = softmax_tile(s, ref, lsum, sl2, pb);
 #pragma unroll
-      for (int d = 0; d < ND; ++d)
+    for (int d = 0; d < ND; ++d)
 #pragma unroll
-        for (int e = 0; e < 16; ++e) o[d][e] *= alpha;
-    }
+      for (int e = 0; e < 16; ++e) o[d][e] *= alpha;
     pv_tile<ND, VS>(sV[0] + voff, pb, o);
     __syncthreads();
   };
@@ -300,7 +300,7 @@ __global__ __launch_bounds__(64 * NW, NW >= 8 ? 1 : 2) void attn_fwd_kernel(Attn
         *reinterpret_cast<bf16x4*>(orow + d * 32 + 8 * i + 4 * hw) = w;
       }
     if (hw == 0 && a.lse != nullptr)
-      a.lse[(size_t)bh * L + qrow] = lt > 0.f ? fmaf(m, a.scale, logf(lt)) : -INFINITY;
+      a.lse[(size_t)bh * L + qrow] = lt > 0.f ? fmaf(ref.m, a.scale, logf(lt)) : -INFINITY;
   }
 }
 
@@ -330,8 +330,10 @@ __global__ __launch_bounds__(64 * NW, NW >= 8 ? 1 : 2) void attn_sparse_pair_ker
   constexpr int ND = D / 32;
   constexpr int NK = D / 16;
   static_assert(VDMA::ELEMS * 2 >= kMaxBlocks, "the V slot holds the block map");
-  __shared__ __attribute__((aligned(1024))) u16 sK[2][KDMA::ELEMS];
-  __shared__ __attribute__((aligned(1024))) u16 sV[2][VDMA::ELEMS];
+  using LD = KVLoader<D, NW>;
+  __shared__ __attribute__((aligned(1024))) u16 sKV[2][LD::ELEMS];   // slots [K | V]
+  const SlotPart<LD::ELEMS, 0> sK{sKV};
+  const SlotPart<LD::ELEMS, LD::VOFF> sV{sKV};
 
   int bh, pq;
   if (a.xcd_map == 1 || a.xcd_map == 3) {
@@ -351,6 +353,7 @@ __global__ __launch_bounds__(64 * NW, NW >= 8 ? 1 : 2) void attn_sparse_pair_ker
   const uint32_t hbytes = (uint32_t)L * D * 2u;
   const __amdgpu_buffer_rsrc_t rK = make_rsrc(a.k + hoff, hbytes);
   const __amdgpu_buffer_rsrc_t rV = make_rsrc(a.v + hoff, hbytes);
+  const u32x4 rKw = rsrc_words(a.k + hoff, hbytes), rVw = rsrc_words(a.v + hoff, hbytes);
   const int qrow = pq * (2 * BLK) + wave * 32 + c32;
   const int voff = ((4 * hw + (gi >> 2)) * VS) * 8 + 16 * (grp & 1) + 4 * (gi & 3);
   const int klane = (c32 * KS + hw) * 8;
@@ -466,8 +469,8 @@ __global__ __launch_bounds__(64 * NW, NW >= 8 ? 1 : 2) void attn_sparse_pair_ker
   };
 
   const float sl2 = a.scale_log2;
-  const float thr = kRescaleLog2 / sl2;
-  float m = -INFINITY, lsum = 0.f;
+  RowRef ref;
+  float lsum = 0.f;
   f32x16 o[ND];
 #pragma unroll
   for (int d = 0; d < ND; ++d) o[d] = f32x16{};
@@ -505,40 +508,51 @@ __global__ __launch_bounds__(64 * NW, NW >= 8 ? 1 : 2) void attn_sparse_pair_ker
       for (int s2 = 0; s2 < 2; ++s2) p_prev[g][s2] = bf16x8{};
     bool pend = false;
     float pend_alpha = 1.f;
-    KVLoader<D, NW> ld;
+    LD ld;
     ld.init(wave, lane);
+    const u32x4 rMw = ld.mixed_v ? rVw : rKw;     // resource of this wave's mixed entry
 
-    // Step t reads K(t+1) and V(t-1) and loads K(t+2) and V(t), as in
-    // attn_fwd_kernel; tile j is union entry j.
-    auto step = [&](int t, const u16* rdK, const u16* rdV, u16* ldK, u16* ldV) {
-      if (pend) {
+    // Step t reads K(t+1) and V(t-1) from slot RS and loads K(t+2) and V(t)
+    // into the other slot, as in attn_fwd_kernel (the K index clamped to the
+    // last tile past the end); tile j is union entry j.
+    auto step = [&](int t, auto rs_c) {
+      constexpr int RS = decltype(rs_c)::value;
+      const u16* rdK = sK[RS];
+      const u16* rdV = sV[RS];
+      if (pend) {             // the reference moved at the previous step
 #pragma unroll
         for (int d = 0; d < ND; ++d)
 #pragma unroll
           for (int e = 0; e < 16; ++e) o[d][e] *= pend_alpha;
+        pend = false;
       }
-      const bool kload = t + 2 < nf;
-      uint32_t kbyte = kload ? (uint32_t)tile_row(t + 2) * (uint32_t)(D * 2) : 0u;
+      uint32_t kbyte = (uint32_t)tile_row(t + 2 < nf ? t + 2 : nf - 1) * (uint32_t)(D * 2);
       uint32_t vbyte = (uint32_t)tile_row(t) * (uint32_t)(D * 2);
       asm volatile("" : "+s"(kbyte), "+s"(vbyte));
-      int wv = wave;
-      asm volatile("" : "+s"(wv));
+      u16* ldK = sK[1 - RS];
+      u16* ldV = sV[1 - RS];
+      uint32_t fill = lds_addr(sKV[1 - RS]);
+      asm volatile("" : "+s"(fill));
+      const uint32_t mbyte = ld.mixed_v ? vbyte : kbyte;
       auto loads = [&](int slot) {
-        constexpr int PK = KVLoader<D, NW>::PWK, NTOT = PK + KVLoader<D, NW>::PWV;
-        constexpr int NM = 2 * NK + 4 * ND;
-        static_assert(NTOT <= NM, "one load instruction per slot at most");
-        const int n = (slot * NTOT + NM - 1) / NM;
-        if (n >= NTOT || (n * NM) / NTOT != slot) return;
-        if (n < PK) {
-          if (kload) ld.k(rK, ldK, kbyte, n, wv);
-        } else {
-          ld.v(rV, ldV, vbyte, n - PK, wv);
-        }
+        constexpr int PW = LD::PW, NM = 2 * NK + 4 * ND;
+        static_assert(PW <= NM, "one load instruction per slot at most");
+        const int n = (slot * PW + NM - 1) / NM;
+        if (n >= PW || (n * NM) / PW != slot) return;
+        ld.issue_n(n, fill, rKw, rVw, rMw, kbyte, vbyte, mbyte);
       };
       f32x16 s_next[2];
       bf16x8 p_cur[2][2];
-      pipelined_step<D, KS, VS>(loads, rdK + klane, rdV + voff, qf, s_cur, p_prev, s_next, p_cur, o, m,
-                                lsum, thr, sl2, pend_alpha, pend);
+      float ts;
+      pipelined_step<D, KS, VS>(loads, rdK + klane, rdV + voff, qf, s_cur, p_prev, s_next, p_cur, o, sl2,
+                                ref.mc, ts);
+      if (__any(ts > ref.lim)) {          // rare: the reference moves for this tile
+        pend_alpha = ref.raise(s_cur, sl2);
+        pend = true;
+        lsum *= pend_alpha;
+        ts = exp_tile(s_cur, sl2, ref.mc, p_cur);
+      }
+      lsum += ts;
 #pragma unroll
       for (int g = 0; g < 2; ++g) {
         s_cur[g] = s_next[g];
@@ -559,10 +573,10 @@ __global__ __launch_bounds__(64 * NW, NW >= 8 ? 1 : 2) void attn_sparse_pair_ker
     };
     int t = 0;
     for (; t + 1 < nf; t += 2) {
-      step(t, sK[1], sV[1], sK[0], sV[0]);
-      step(t + 1, sK[0], sV[0], sK[1], sV[1]);
+      step(t, std::integral_constant<int, 1>{});
+      step(t + 1, std::integral_constant<int, 0>{});
     }
-    if (t < nf) step(t, sK[1], sV[1], sK[0], sV[0]);
+    if (t < nf) step(t, std::integral_constant<int, 1>{});
     if (pend) {
 #pragma unroll
       for (int d = 0; d < ND; ++d)
@@ -584,15 +598,11 @@ __global__ __launch_bounds__(64 * NW, NW >= 8 ? 1 : 2) void attn_sparse_pair_ker
     mask_tile(s, L - kb, hw);
     if (!(keep & mybit)) hide(s);
     bf16x8 pb[2][2];
-    float alpha;
-    bool moved;
-    softmax_tile(s, m, lsum, thr, sl2, pb, alpha, moved);
-    if (moved) {
+    const float alpha = softmax_tile(s, ref, lsum, sl2, pb);
 #pragma unroll
-      for (int d = 0; d < ND; ++d)
+    for (int d = 0; d < ND; ++d)
 #pragma unroll
-        for (int e = 0; e < 16; ++e) o[d][e] *= alpha;
-    }
+      for (int e = 0; e < 16; ++e) o[d][e] *= alpha;
     pv_tile<ND, VS>(sV[0] + voff, pb, o);
     __syncthreads();
   };
@@ -630,7 +640,7 @@ __global__ __launch_bounds__(64 * NW, NW >= 8 ? 1 : 2) void attn_sparse_pair_ker
         *reinterpret_cast<bf16x4*>(orow + d * 32 + 8 * i + 4 * hw) = w;
       }
     if (hw == 0 && a.lse != nullptr)
-      a.lse[(size_t)bh * L + qrow] = lt > 0.f ? fmaf(m, a.scale, logf(lt)) : -INFINITY;
+      a.lse[(size_t)bh * L + qrow] = lt > 0.f ? fmaf(ref.m, a.scale, logf(lt)) : -INFINITY;
   }
 }
 

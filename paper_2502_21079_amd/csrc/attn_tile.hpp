@@ -11,10 +11,11 @@
 // the 16 keys of each MFMA step are ordered to match the accumulator rows; the
 // V^T operand is read from a row-major V tile with the LDS transpose read.
 //
-// Online softmax.  The reference max of a row moves only when a tile's max
-// exceeds it by more than 2^8 in the exp2 domain (checked per 32 rows), so the
-// rescale of the output accumulator is skipped for almost every tile; the
-// final normalisation uses the same reference, so the result is unchanged.
+// Online softmax.  Probabilities are taken against a per-row reference that
+// moves only when a tile's probabilities grow too large (checked per 32 rows
+// from their sum), so neither a per-tile maximum nor a rescale of the output
+// accumulator is needed for almost every tile; the final normalisation uses
+// the same reference, so the result is unchanged.
 #pragma once
 
 #include <type_traits>
@@ -25,7 +26,6 @@
 namespace adaspa {
 
 constexpr int KT = 64;          // keys per tile
-constexpr float kRescaleLog2 = 8.f;
 
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
@@ -33,6 +33,40 @@ typedef __attribute__((address_space(3))) void lds_void;
 
 __device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void* base, uint32_t bytes) {
   return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), 0, bytes, 0x00020000);
+}
+
+// Buffer resource words (base, stride 0, size in bytes, the format word of
+// make_rsrc) in scalar registers, for the loads issued by dma16.
+__device__ __forceinline__ u32x4 rsrc_words(const void* base, uint32_t bytes) {
+  const uint64_t b = (uint64_t)base;
+  u32x4 r;
+  r.x = __builtin_amdgcn_readfirstlane((uint32_t)b);
+  r.y = __builtin_amdgcn_readfirstlane((uint32_t)(b >> 32));
+  r.z = __builtin_amdgcn_readfirstlane(bytes);
+  r.w = 0x00020000u;
+  return r;
+}
+
+// One 16-byte-per-lane direct load into LDS: lane l's 16 bytes at voff +
+// soff of the buffer go to LDS byte lds + OFS + 16 l.  It is issued as inline
+// asm so that the compiler does not track it: otherwise it makes every later
+// LDS read wait for the load (vmcnt) unless it can prove the two touch
+// different addresses, which it cannot for the ring slots.  The ordering is
+// explicit instead: a loaded tile is read only after a vmcnt(0) wait and a
+// barrier, and a slot is refilled only after the barrier that follows its
+// last read.  M0 carries the LDS address; the compiler sets M0 itself before
+// each of its own uses, so clobbering it here is harmless.
+#pragma clang diagnostic push
+#pragma clang diagnostic ignored "-Winline-asm"
+template <int OFS>
+__device__ __forceinline__ void dma16(u32x4 rsrc, uint32_t lds, uint32_t voff, uint32_t soff) {
+  asm volatile("s_add_u32 m0, %0, %4\n\ts_nop 0\n\tbuffer_load_dwordx4 %1, %2, %3 offen lds"
+               :: "s"(lds), "v"(voff), "s"(rsrc), "s"(soff), "n"(OFS) : "m0");
+}
+#pragma clang diagnostic pop
+
+__device__ __forceinline__ uint32_t lds_addr(const void* p) {
+  return (uint32_t)(size_t)(const __attribute__((address_space(3))) void*)p;
 }
 
 // One [KT, D] bf16 tile in LDS with padded rows: row r starts at chunk
@@ -109,40 +143,80 @@ struct KLoader {
 };
 
 
-// Loads of one full K tile and one full V tile spread over a step.  Wave w
-// owns instructions i = j * NW + w of each tile; the two 16-bit in-tile
-// offsets of instruction j are kept packed in one register (K low, V high).
+// Loads of one full K tile and one full V tile per step into one ring slot
+// laid out [K tile | V tile].  The 64-slot DMA instructions of the two tiles
+// form one list of NTOT = K::NINST + V::NINST entries, entry f writing the
+// f-th 1 KB piece of the slot, and wave w issues entry j * NW + w for j = 0
+// .. PW-1.  Every wave issues the same number of loads and none sits behind
+// a branch: where the list runs out (the last j of some waves) a wave repeats
+// its entry of j - 1 (the same data to the same place).  The source of a load
+// is the tile's first byte (scalar offset) plus a per-lane in-tile offset kept
+// in a register, and its destination the slot plus a per-wave constant.
+// Entries j with (j+1)*NW <= K::NINST are K loads for every wave, entries
+// with j*NW >= K::NINST are V loads for every wave, and the one j in between
+// (if any) is K for some waves and V for the others ("mixed").
 template <int D, int NW>
 struct KVLoader {
   using K = TileDMA<D, NW, 1>;
   using V = TileDMA<D, NW, 2>;
-  static constexpr int PWK = (K::NINST + NW - 1) / NW;
-  static constexpr int PWV = (V::NINST + NW - 1) / NW;
-  static constexpr int PW = PWK > PWV ? PWK : PWV;
+  static constexpr int NK = K::NINST;
+  static constexpr int NTOT = K::NINST + V::NINST;
+  static constexpr int PW = (NTOT + NW - 1) / NW;           // loads per wave and step
+  static constexpr int ELEMS = K::ELEMS + V::ELEMS;         // bf16 elements per ring slot
+  static constexpr int VOFF = K::ELEMS;                     // V tile within the slot
+  static_assert(K::ELEMS == NK * 512, "the V tile starts right after the K tile's pieces");
+  static_assert(V::NINST >= NW, "a repeated entry must be a V load of the same wave");
+  static_assert(NK % NW == 0 || NK / NW != PW - 1, "the mixed entry is not the last one");
   static_assert(KT * D * 2 <= 65536, "in-tile offsets must fit in 16 bits");
-  uint32_t rel[PW];
+  static constexpr bool all_k(int j) { return (j + 1) * NW <= NK; }
+  static constexpr bool all_v(int j) { return j * NW >= NK; }
+
+  uint32_t rel[PW];          // per lane: in-tile source offset of load j
+  uint32_t wbase;            // LDS byte offset of this wave's piece of entry j = 0
+  uint32_t wlast;            // the same for the last entry (one row of pieces lower if it repeats)
+  bool mixed_v;              // the mixed entry is a V load for this wave
 
   __device__ __forceinline__ void init(int wave, int lane) {
+    wbase = (uint32_t)wave * 1024u;
+    wlast = wbase - (((PW - 1) * NW + wave >= NTOT) ? (uint32_t)NW * 1024u : 0u);
+    mixed_v = (NK / NW) * NW + wave >= NK;
 #pragma unroll
     for (int j = 0; j < PW; ++j) {
-      const int i = j * NW + wave;
-      const uint32_t k = i < K::NINST ? K::rel_offset(i, lane) : 0u;
-      const uint32_t v = i < V::NINST ? V::rel_offset(i, lane) : 0u;
-      rel[j] = k | (v << 16);
+      int f = j * NW + wave;
+      if (f >= NTOT) f -= NW;
+      rel[j] = f < NK ? K::rel_offset(f, lane) : V::rel_offset(f - NK, lane);
     }
   }
-  __device__ __forceinline__ void k(__amdgpu_buffer_rsrc_t r, u16* dst, uint32_t tile_byte, int j,
-                                    int wave) const {
-    const int i = j * NW + wave;
-    if (j < PWK && i < K::NINST) K::issue_full(r, dst, tile_byte, i, rel[j] & 0xFFFFu);
+  // Load J of this wave into the slot at LDS byte address slot; rK / rV are
+  // the K and V resources and rM the one of this wave's mixed entry, kbyte /
+  // vbyte / mbyte the first bytes of the K tile, the V tile and the mixed
+  // entry's tile.
+  template <int J>
+  __device__ __forceinline__ void issue(uint32_t slot, u32x4 rK, u32x4 rV, u32x4 rM, uint32_t kbyte,
+                                        uint32_t vbyte, uint32_t mbyte) const {
+    constexpr int F = J * NW * 1024;
+    if constexpr (J == PW - 1) dma16<F>(rV, slot + wlast, rel[J], vbyte);
+    else if constexpr (all_k(J)) dma16<F>(rK, slot + wbase, rel[J], kbyte);
+    else if constexpr (all_v(J)) dma16<F>(rV, slot + wbase, rel[J], vbyte);
+    else dma16<F>(rM, slot + wbase, rel[J], mbyte);
   }
-  __device__ __forceinline__ void v(__amdgpu_buffer_rsrc_t r, u16* dst, uint32_t tile_byte, int j,
-                                    int wave) const {
-    const int i = j * NW + wave;
-    if (j < PWV && i < V::NINST) V::issue_full(r, dst, tile_byte, i, rel[j] >> 16);
+  // Load n (a constant once the caller's loop is unrolled).
+  template <int J = 0>
+  __device__ __forceinline__ void issue_n(int n, uint32_t slot, u32x4 rK, u32x4 rV, u32x4 rM, uint32_t kbyte,
+                                          uint32_t vbyte, uint32_t mbyte) const {
+    if constexpr (J < PW) {
+      if (n == J) issue<J>(slot, rK, rV, rM, kbyte, vbyte, mbyte);
+      else issue_n<J + 1>(n, slot, rK, rV, rM, kbyte, vbyte, mbyte);
+    }
   }
 };
 
+// The K or V part of the ring slots: part[b] is the tile in slot b.
+template <int ELEMS, int OFF>
+struct SlotPart {
+  u16 (*slots)[ELEMS];
+  __device__ __forceinline__ u16* operator[](int b) const { return slots[b] + OFF; }
+};
 
 // Maximum without the sNaN canonicalisation that fmaxf needs in IEEE mode
 // (a NaN score propagates, which is fine: the row is then NaN either way).
@@ -199,45 +273,77 @@ __device__ __forceinline__ void zero_lds(u16* p, int tid, int nt) {
   for (int i = tid; i < NCH; i += nt) *reinterpret_cast<u32x4*>(p + i * 8) = u32x4{0, 0, 0, 0};
 }
 
-// Online softmax of one S^T tile (log2 domain).  The reference max m moves
-// only when some row of the wave exceeds it by more than kRescaleLog2; then
-// alpha = exp2((m_old - m_new) * sl2) rescales the running sum here and the
-// output accumulator later (moved tells the caller).  P is returned in bf16
-// and the running sum adds exactly those rounded values, so numerator and
-// denominator use the same weights.
-__device__ __forceinline__ void softmax_tile(const f32x16 (&s)[2], float& m, float& lsum, float thr,
-                                             float sl2, bf16x8 (&pb)[2][2], float& alpha,
-                                             bool& moved) {
-  float mt = -INFINITY;
+// Online softmax against a lazy reference.  Probabilities of a row are taken
+// as exp2(s * sl2 - mc) with mc = m * sl2 for a reference m (raw score units)
+// that is NOT the running maximum: it moves only when the probabilities of a
+// tile, summed over one lane's keys, exceed kTileSumLimit (or are positive at
+// all while m is still -inf), so no per-tile maximum is computed.  Every
+// probability then stays below 2^16 (no overflow of the fp32 sums), and the
+// final normalisation uses the same reference, so the result is the softmax
+// whatever the reference.  When the reference moves, sums taken against the
+// old one are rescaled by exp2((m_old - m_new) * sl2).
+constexpr float kTileSumLimit = 65536.f;
+
+struct RowRef {
+  float m = -INFINITY;   // reference, raw score units; -inf until a finite score is seen
+  float mc = 0.f;        // m * sl2 (0 while m is -inf)
+  float lim = 0.f;       // tile sum above which the reference must move
+
+  // m <- max(m, row maximum of s) for the rows of this wave (the two
+  // half-waves holding a row agree); returns the rescale factor of sums
+  // taken against the old reference.
+  __device__ __forceinline__ float raise(const f32x16 (&s)[2], float sl2) {
+    float mt = -INFINITY;
 #pragma unroll
-  for (int g = 0; g < 2; ++g)
+    for (int g = 0; g < 2; ++g)
 #pragma unroll
-    for (int e = 0; e < 16; e += 2) mt = vmax(mt, vmax(s[g][e], s[g][e + 1]));
-  {
+      for (int e = 0; e < 16; e += 2) mt = vmax(mt, vmax(s[g][e], s[g][e + 1]));
     float lo, hi;
     half_pair(mt, lo, hi);
     mt = vmax(lo, hi);
+    const float mnew = fmaxf(m, mt);
+    const float a = (mnew == -INFINITY) ? 1.f : fast_exp2((m - mnew) * sl2);
+    m = mnew;
+    mc = (m == -INFINITY) ? 0.f : m * sl2;
+    lim = (m == -INFINITY) ? 0.f : kTileSumLimit;
+    return a;
   }
-  moved = __any(mt > m + thr);
-  const float mnew = moved ? fmaxf(m, mt) : m;
-  alpha = (mnew == -INFINITY) ? 1.f : fast_exp2((m - mnew) * sl2);
-  lsum *= alpha;
-  m = mnew;
-  const float mc = (m == -INFINITY) ? 0.f : m * sl2;
-#pragma unroll
-  for (int g = 0; g < 2; ++g)
-#pragma unroll
-    for (int e = 0; e < 16; ++e) pb[g][e >> 3][e & 7] = (__bf16)fast_exp2(fmaf(s[g][e], sl2, -mc));
+};
+
+// P = bf16(exp2(s * sl2 - mc)) for one S^T tile; returns this lane's sum of
+// exactly the rounded values that enter P V, so numerator and denominator
+// use the same weights.
+__device__ __forceinline__ float exp_tile(const f32x16 (&s)[2], float sl2, float mc, bf16x8 (&pb)[2][2]) {
   const bf16x2 ones = {(__bf16)1.0f, (__bf16)1.0f};
+  float ts = 0.f;
 #pragma unroll
   for (int g = 0; g < 2; ++g)
 #pragma unroll
-    for (int s2 = 0; s2 < 2; ++s2)
-#pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        const bf16x2 pr = {pb[g][s2][2 * j], pb[g][s2][2 * j + 1]};
-        lsum = __builtin_amdgcn_fdot2_f32_bf16(pr, ones, lsum, false);
-      }
+    for (int e = 0; e < 16; e += 2) {
+      const bf16x2 pr = {(__bf16)fast_exp2(fmaf(s[g][e], sl2, -mc)),
+                         (__bf16)fast_exp2(fmaf(s[g][e + 1], sl2, -mc))};
+      pb[g][e >> 3][e & 7] = pr[0];
+      pb[g][e >> 3][(e & 7) + 1] = pr[1];
+      ts = __builtin_amdgcn_fdot2_f32_bf16(pr, ones, ts, false);
+    }
+  return ts;
+}
+
+// Softmax of one tile outside the pipeline (masked tiles): P against the
+// current reference, moved first if this tile needs it.  Returns the factor
+// by which the output accumulator must be rescaled before this tile's P V
+// (1 when the reference did not move); lsum includes the tile afterwards.
+__device__ __forceinline__ float softmax_tile(const f32x16 (&s)[2], RowRef& ref, float& lsum, float sl2,
+                                              bf16x8 (&pb)[2][2]) {
+  float ts = exp_tile(s, sl2, ref.mc, pb);
+  float a = 1.f;
+  if (__any(ts > ref.lim)) {
+    a = ref.raise(s, sl2);
+    lsum *= a;
+    ts = exp_tile(s, sl2, ref.mc, pb);
+  }
+  lsum += ts;
+  return a;
 }
 
 // O^T += V^T P^T for one tile.  MFMA step (g, s2) covers keys
@@ -267,28 +373,26 @@ __device__ __forceinline__ void pv_tile(const u16* vlane, const bf16x8 (&pb)[2][
 // of the previous tile).  The QK MFMAs alternate between the two 32-key score
 // groups and the PV MFMAs rotate over the ND output blocks, so two MFMAs into
 // the same accumulator are 4 (QK) or 2*ND (PV) slots apart and one wave alone
-// keeps the matrix pipe busy; each accumulator still sums in the same order.  Each slot first issues the LDS operand reads of the
-// slot LA places ahead, then its MFMA, then hook(slot) (the caller's tile
-// loads, spread over the step so the load path never stalls the wave for
-// long), then a fixed slice of the softmax of the current tile; a scheduling
-// fence closes the slot, so the matrix pipe and the VALU work side by side
-// within the wave.
+// keeps the matrix pipe busy; each accumulator still sums in the same order.
+// Each slot first issues the LDS operand reads of the slot LA places ahead,
+// then its MFMA, then hook(slot) (the caller's tile loads, spread over the
+// step so the load path never stalls the wave for long), then an equal share
+// of the exponentials of the current tile against the reference mc; a
+// scheduling fence closes the slot, so the matrix pipe and the VALU work side
+// by side within the wave.  tsum returns this lane's sum of the tile's
+// rounded probabilities; the caller checks it against the reference's limit.
 template <int D, int KS, int VS, typename Hook>
 __device__ __forceinline__ void pipelined_step(Hook&& hook, const u16* klane, const u16* vlane,
                                                const bf16x8 (&qf)[D / 16], const f32x16 (&s_cur)[2],
                                                const bf16x8 (&p_prev)[2][2], f32x16 (&s_next)[2],
-                                               bf16x8 (&p_cur)[2][2], f32x16 (&o)[D / 32], float& m,
-                                               float& lsum, float thr, float sl2, float& alpha,
-                                               bool& moved) {
+                                               bf16x8 (&p_cur)[2][2], f32x16 (&o)[D / 32], float sl2,
+                                               float mc, float& tsum) {
   constexpr int NK = D / 16, ND = D / 32;
   constexpr int NQK = 2 * NK, NPV = 4 * ND;
   static_assert(NQK == NPV, "QK and PV slots alternate");
   constexpr int NM = NQK + NPV;
+  static_assert(32 % NM == 0 && NM % 2 == 0, "whole exponential pairs per slot pair");
   constexpr int LA = 2;                       // operand lookahead, in slots
-  constexpr int P1_END = NM / 4;              // max reduction in slots [0, P1_END)
-  constexpr int SHFL = P1_END;                // cross-half max exchange
-  constexpr int MC = P1_END + 2;              // reference update
-  constexpr int P2 = MC + 1;                  // exponentials in slots [P2, NM)
 
   bf16x8 op[NM];
   auto fetch = [&](int i) {
@@ -317,48 +421,26 @@ __device__ __forceinline__ void pipelined_step(Hook&& hook, const u16* klane, co
     }
   };
 
-  float mt = -INFINITY, mtl = -INFINITY, mth = -INFINITY, mc = 0.f;
   const bf16x2 ones = {(__bf16)1.0f, (__bf16)1.0f};
+  float ts = 0.f, x0 = 0.f;
   auto valu = [&](int i) {
-    if (i < P1_END) {
-      // 16 max3 over the 32 scores, spread over the first P1_END slots
-      constexpr int PER = 16 / P1_END;
+    // scores e in [i*32/NM, (i+1)*32/NM) of the tile's 32, in (group,
+    // element) order; a pair is rounded to bf16 and summed once complete.
+    constexpr int PER = 32 / NM;
 #pragma unroll
-      for (int u = 0; u < PER; ++u) {
-        const int q = i * PER + u;          // pair index 0..15
-        const int g = q >> 3, e = (q & 7) * 2;
-        mt = vmax(mt, vmax(s_cur[g][e], s_cur[g][e + 1]));
+    for (int u = 0; u < PER; ++u) {
+      const int e = i * PER + u, g = e >> 4, r = e & 15;
+      const float x = fast_exp2(fmaf(s_cur[g][r], sl2, -mc));
+      if ((e & 1) == 0) {
+        x0 = x;
+        pin(x0);
+      } else {
+        const bf16x2 pr = {(__bf16)x0, (__bf16)x};
+        p_cur[g][r >> 3][(r & 7) - 1] = pr[0];
+        p_cur[g][r >> 3][r & 7] = pr[1];
+        ts = __builtin_amdgcn_fdot2_f32_bf16(pr, ones, ts, false);
+        pin(ts);
       }
-      pin(mt);
-    } else if (i == SHFL) {
-      half_pair(mt, mtl, mth);
-    } else if (i == MC) {
-      mt = vmax(mtl, mth);
-      moved = __any(mt > m + thr);
-      const float mnew = moved ? fmaxf(m, mt) : m;
-      alpha = (mnew == -INFINITY) ? 1.f : fast_exp2((m - mnew) * sl2);
-      lsum *= alpha;
-      m = mnew;
-      mc = (m == -INFINITY) ? 0.f : m * sl2;
-      pin(mc);
-    } else if (i >= P2) {
-      // 32 exponentials in groups of 4 (one bf16x4 quarter of p_cur)
-      constexpr int NQ = 8;                   // quarters of 4 elements
-      const int k = i - P2;                   // 0 .. NM - P2 - 1
-      const int q0 = k * NQ / (NM - P2), q1 = (k + 1) * NQ / (NM - P2);
-#pragma unroll
-      for (int q = q0; q < q1; ++q) {         // quarter q: g = q/4, elements 4*(q%4)..+3
-        const int g = q >> 2, e0 = (q & 3) * 4;
-#pragma unroll
-        for (int e = e0; e < e0 + 4; ++e)
-          p_cur[g][e >> 3][e & 7] = (__bf16)fast_exp2(fmaf(s_cur[g][e], sl2, -mc));
-#pragma unroll
-        for (int e = e0; e < e0 + 4; e += 2) {
-          const bf16x2 pr = {p_cur[g][e >> 3][e & 7], p_cur[g][e >> 3][(e & 7) + 1]};
-          lsum = __builtin_amdgcn_fdot2_f32_bf16(pr, ones, lsum, false);
-        }
-      }
-      pin(lsum);
     }
   };
 
@@ -372,6 +454,7 @@ __device__ __forceinline__ void pipelined_step(Hook&& hook, const u16* klane, co
     valu(i);
     __builtin_amdgcn_sched_barrier(0);
   }
+  tsum = ts;
 }
 
 // One pipelined step of the block-mass pass: the NM = 2*NK QK MFMAs of the
