@@ -111,13 +111,26 @@ typedef struct {
 /* Human-readable name of a status code (static storage). */
 const char* adaspa_status_string(adaspa_status s);
 
+/* Device bytes of the optional workspace of adaspa_dense_attn_lse (0 for
+ * invalid arguments). */
+size_t adaspa_dense_attn_workspace(const adaspa_problem* prob);
+
 /* Dense attention with LSE (Sec. 2.2; Algorithm 1, first pass).
  *   out[b,h,i,:] = sum_j softmax_j(scale * q_i . k_j) v_j        bf16 (RNE)
  *   lse[b,h,i]   = log sum_j exp(scale * q_i . k_j)             fp32
- * q, k, v, out: bf16 [B,H,L,D]; lse: fp32 [B,H,L] (may be NULL to skip). */
+ * q, k, v, out: bf16 [B,H,L,D]; lse: fp32 [B,H,L] (may be NULL to skip).
+ * workspace (optional, caller-owned, 16-byte aligned, at least
+ * adaspa_dense_attn_workspace() bytes, contents need not be initialised)
+ * holds the counters of a work queue per XCD, so that the XCDs that run
+ * faster take more of the work; with NULL the work is split statically.  The
+ * results are bitwise the same either way.  The call clears the counters
+ * itself (with a kernel on `stream`); calls that may run concurrently need
+ * separate workspaces.  ADASPA_ERR_WORKSPACE if it is too small or
+ * misaligned. */
 adaspa_status adaspa_dense_attn_lse(const adaspa_problem* prob, const void* q,
                                     const void* k, const void* v, void* out,
-                                    float* lse, void* stream);
+                                    float* lse, void* workspace,
+                                    size_t workspace_bytes, void* stream);
 
 /* Device bytes of workspace adaspa_block_search needs for this problem and
  * selection (0 for invalid arguments). */

@@ -22,14 +22,14 @@ from typing import Optional, Sequence
 
 import torch
 
-__all__ = ["dense_attn_lse", "block_search", "block_sparse_attn", "SearchResult",
+__all__ = ["dense_attn_lse", "dense_attn_workspace", "block_search", "block_sparse_attn", "SearchResult",
            "library_path", "load_library", "AdaspaError", "EXPORTED_SYMBOLS",
            "block_search_workspace", "block_search_capacity"]
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
 _LIB_NAME = "libadaspa.so"
 
-EXPORTED_SYMBOLS = ("adaspa_status_string", "adaspa_dense_attn_lse",
+EXPORTED_SYMBOLS = ("adaspa_status_string", "adaspa_dense_attn_workspace", "adaspa_dense_attn_lse",
                     "adaspa_block_search_workspace", "adaspa_block_search_capacity",
                     "adaspa_block_search", "adaspa_block_sparse_attn")
 
@@ -78,8 +78,10 @@ def load_library():
     vp, i32p, f32p = ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p
     lib.adaspa_status_string.restype = ctypes.c_char_p
     lib.adaspa_status_string.argtypes = [ctypes.c_int]
+    lib.adaspa_dense_attn_workspace.restype = ctypes.c_size_t
+    lib.adaspa_dense_attn_workspace.argtypes = [P]
     lib.adaspa_dense_attn_lse.restype = ctypes.c_int
-    lib.adaspa_dense_attn_lse.argtypes = [P, vp, vp, vp, vp, f32p, vp]
+    lib.adaspa_dense_attn_lse.argtypes = [P, vp, vp, vp, vp, f32p, vp, ctypes.c_size_t, vp]
     lib.adaspa_block_search_workspace.restype = ctypes.c_size_t
     lib.adaspa_block_search_workspace.argtypes = [P, S]
     lib.adaspa_block_search_capacity.restype = ctypes.c_int64
@@ -137,8 +139,14 @@ def _select(mode: str, head_param_bp: Optional[Sequence[int]], text_sink: bool,
 
 
 def dense_attn_lse(q, k, v, *, scale: Optional[float] = None, out=None, lse=None,
-                   want_lse: bool = True):
-    """Dense attention and per-row natural-log LSE.  Returns (out, lse)."""
+                   want_lse: bool = True, workspace=None, balance: bool = True):
+    """Dense attention and per-row natural-log LSE.  Returns (out, lse).
+
+    With ``balance`` (the default) the XCDs share the work through per-XCD
+    work queues whose counters live in ``workspace`` (uint8 CUDA tensor of at
+    least ``dense_attn_workspace(q.shape)`` bytes; allocated here when not
+    given); ``balance=False`` splits the work statically.  The results are
+    the same either way."""
     _check_qkv(q, k, v)
     lib = load_library()
     B, H, L, D = q.shape
@@ -147,9 +155,25 @@ def dense_attn_lse(q, k, v, *, scale: Optional[float] = None, out=None, lse=None
     if lse is None and want_lse:
         lse = torch.empty(B, H, L, dtype=torch.float32, device=q.device)
     prob = _problem(q, 128, 0, 0, scale)
+    ws_bytes = 0
+    if balance:
+        ws_bytes = int(lib.adaspa_dense_attn_workspace(ctypes.byref(prob)))
+        if workspace is None:
+            workspace = torch.empty(ws_bytes, dtype=torch.uint8, device=q.device)
+        ws_bytes = workspace.numel() * workspace.element_size()
+    else:
+        workspace = None
     _check(lib.adaspa_dense_attn_lse(ctypes.byref(prob), _ptr(q), _ptr(k), _ptr(v), _ptr(out),
-                                     _ptr(lse), _stream(q.device)))
+                                     _ptr(lse), _ptr(workspace), ctypes.c_size_t(ws_bytes),
+                                     _stream(q.device)))
     return out, lse
+
+
+def dense_attn_workspace(shape, scale: Optional[float] = None) -> int:
+    """Bytes of the work-queue workspace of :func:`dense_attn_lse`."""
+    B, H, L, D = shape
+    prob = _Problem(B, H, L, D, 128, 0, 0, 0.0 if scale is None else float(scale))
+    return int(load_library().adaspa_dense_attn_workspace(ctypes.byref(prob)))
 
 
 @dataclass

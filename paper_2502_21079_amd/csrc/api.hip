@@ -149,14 +149,22 @@ const char* adaspa_status_string(adaspa_status s) {
   return "unknown status";
 }
 
+size_t adaspa_dense_attn_workspace(const adaspa_problem* prob) {
+  if (check_problem(prob) != ADASPA_OK) return 0;
+  return kAlign;   // eight 32-bit work-queue counters, padded
+}
+
 adaspa_status adaspa_dense_attn_lse(const adaspa_problem* prob, const void* q, const void* k,
-                                    const void* v, void* out, float* lse, void* stream) {
+                                    const void* v, void* out, float* lse, void* workspace,
+                                    size_t workspace_bytes, void* stream) {
   adaspa_status st = check_problem(prob);
   if (st != ADASPA_OK) return st;
   if (!q || !k || !v || !out) return ADASPA_ERR_INVALID_ARG;
   if (!aligned16(q) || !aligned16(k) || !aligned16(v) || !aligned16(out) ||
       (lse && ((uintptr_t)lse & 3u)))
     return ADASPA_ERR_INVALID_ARG;
+  if (workspace && (workspace_bytes < adaspa_dense_attn_workspace(prob) || !aligned16(workspace)))
+    return ADASPA_ERR_WORKSPACE;
   AttnParams a;
   memset(&a, 0, sizeof a);
   a.q = (const u16*)q;
@@ -171,6 +179,7 @@ adaspa_status adaspa_dense_attn_lse(const adaspa_problem* prob, const void* q, c
   a.scale = scale_of(prob);
   a.scale_log2 = a.scale * 1.4426950408889634f;
   a.xcd_map = xcd_map_mode(1);
+  a.claim = (uint32_t*)workspace;
   return launch_dense(a, prob->head_dim, (hipStream_t)stream) == hipSuccess ? ADASPA_OK : ADASPA_ERR_HIP;
 }
 

@@ -9,6 +9,35 @@
 
 namespace adaspa {
 
+// Dynamic work distribution over the XCDs.  The XCDs of one chip do not run
+// at the same speed (per-XCD step times differ by up to ~10% on the same
+// work), so a static equal split leaves the fast ones idle at the end.  Work
+// item i (in the kernel's static order) belongs to the queue of XCD i % 8, as
+// the hardware's round-robin dispatch would place it; a workgroup takes the
+// next item of its own XCD's queue with an atomic increment and, once that is
+// empty, the next item of another queue, and exits when all are empty.  The
+// grid has more workgroups than items, so a faster XCD simply runs more of
+// them.  Items keep their order within a queue, so neighbouring tiles still
+// share an L2.
+__device__ __forceinline__ int xcc_id() {
+  return __builtin_amdgcn_s_getreg(20 | (0 << 6) | (3 << 11)) & 7;   // HW_REG_XCC_ID[3:0]
+}
+
+__device__ __forceinline__ int claim_item(uint32_t* ctr, int n) {
+  const int x = xcc_id();
+  for (int k = 0; k < 8; ++k) {
+    const int y = (x + k) & 7;
+    const int m = (n - y + 7) / 8;            // items of queue y
+    const unsigned j = atomicAdd(&ctr[y], 1u);
+    if ((int)j < m) return (int)j * 8 + y;
+  }
+  return -1;
+}
+
+__global__ void claim_reset_kernel(uint32_t* ctr) {
+  if (threadIdx.x < 8) ctr[threadIdx.x] = 0u;
+}
+
 // ---------------------------------------------------------------------------
 // Flash attention forward (dense and block-sparse share this body).
 //
@@ -44,6 +73,15 @@ __global__ __launch_bounds__(64 * NW, NW >= 8 ? 1 : 2) void attn_fwd_kernel(Attn
     xcd_chunk_map(blockIdx.x, a.nqt, a.batch_heads, bh, qt);
   } else if (SPARSE && (a.xcd_map == 1 || a.xcd_map == 3)) {
     text_first_map(blockIdx.x, a.n_wg, a.nqt, a.tq0, a.tq1 - a.tq0, bh, qt, a.xcd_map == 3);
+  } else if (!SPARSE && a.claim != nullptr) {
+    __shared__ int s_item;
+    if (threadIdx.x == 0) s_item = claim_item(a.claim, a.n_items);
+    __syncthreads();
+    const int item = s_item;
+    if (item < 0) return;                    // every item is taken
+    const int lid = a.xcd_map ? xcd_remap(item, a.n_items) : item;
+    bh = lid / a.nqt;
+    qt = lid % a.nqt;
   } else {
     const int lid = a.xcd_map ? xcd_remap(blockIdx.x, a.n_wg) : (int)blockIdx.x;
     bh = lid / a.nqt;
@@ -686,6 +724,7 @@ __global__ __launch_bounds__(256, 2) void block_mass_kernel(MassParams a) {
   const int L = a.seqlen;
   const size_t hoff = (size_t)bh * L * D;
   const __amdgpu_buffer_rsrc_t rK = make_rsrc(a.k + hoff, (uint32_t)L * D * 2u);
+  const u32x4 rKw = rsrc_words(a.k + hoff, (uint32_t)L * D * 2u);
   const int qrow = pg * 128 + wave * 32 + c32;
   const bool qvalid = qrow < L;
 
@@ -746,15 +785,18 @@ __global__ __launch_bounds__(256, 2) void block_mass_kernel(MassParams a) {
     const int klane = (c32 * KS + hw) * 8;
     // Step t (t + 1 < nfull) sums tile t, forms the scores of tile t+1 from
     // buffer (t+1)&1 and loads tile t+2 into buffer t&1.
+    // Past the last tile the load is clamped to the last one (an in-range
+    // load into a buffer that is not read again), so no load is branched.
     auto step = [&](int t, const u16* rdK, u16* ldK) {
-      const bool kload = t + 2 < nfull;
-      const uint32_t kbyte = (uint32_t)(t + 2) * (uint32_t)(KT * D * 2);
+      const uint32_t kbyte = (uint32_t)(t + 2 < nfull ? t + 2 : nfull - 1) * (uint32_t)(KT * D * 2);
+      uint32_t fill = lds_addr(ldK);
+      asm volatile("" : "+s"(fill));
       auto loads = [&](int slot) {
         constexpr int NTOT = KLoader<D, NW>::PW, NM = 2 * NK;
         static_assert(NTOT <= NM, "one load instruction per slot at most");
         const int n = (slot * NTOT + NM - 1) / NM;
         if (n >= NTOT || (n * NM) / NTOT != slot) return;
-        if (kload) ld.k(rK, ldK, kbyte, n, wave);
+        ld.issue_n(n, fill, rKw, kbyte);
       };
       f32x16 s_next[2];
       mass_step<D, KS>(loads, rdK + klane, qf, s_cur, s_next, acc, sl2, nlse2);
@@ -823,7 +865,18 @@ hipError_t launch_dense(AttnParams a, int D, hipStream_t st) {
   a.row_ptr = nullptr;
   a.col_idx = nullptr;
   a.nqt = (a.seqlen + 255) / 256;
-  a.n_wg = a.nqt * a.batch_heads;
+  a.n_items = a.nqt * a.batch_heads;
+  a.n_wg = a.n_items;
+  if (a.claim != nullptr) {
+    // A quarter more workgroups than items: the XCDs that run ahead take the
+    // items the others have not reached; surplus workgroups find every queue
+    // empty and exit.  The counters are cleared by a kernel (not a memset),
+    // so the pair of launches can be captured in a graph.
+    a.n_wg = a.n_items + (a.n_items + 3) / 4;
+    hipLaunchKernelGGL(claim_reset_kernel, dim3(1), dim3(64), 0, st, a.claim);
+    const hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+  }
   if (D == 64) return launch_attn<64, 8, false>(a, st);
   return launch_attn<128, 8, false>(a, st);
 }

@@ -121,24 +121,36 @@ struct TileDMA {
 };
 using std::integral_constant;
 
-// Loads of one full K tile spread over a step (the block-mass pass).
+// Loads of one full K tile per step (the block-mass pass), uniform over the
+// waves as in KVLoader below: wave w issues the tile's DMA instructions
+// j * NW + w, j = 0 .. PW-1, and repeats its entry of j - 1 where the list
+// runs out, so no load sits behind a branch.
 template <int D, int NW>
 struct KLoader {
   using K = TileDMA<D, NW, 1>;
   static constexpr int PW = (K::NINST + NW - 1) / NW;
-  uint32_t rel[PW];
+  static_assert(K::NINST >= NW, "a repeated entry must be a load of the same wave");
+  uint32_t rel[PW];          // per lane: in-tile source offset of load j
+  uint32_t wbase, wlast;     // LDS byte offsets of this wave's pieces of entries 0 and PW-1
 
   __device__ __forceinline__ void init(int wave, int lane) {
+    wbase = (uint32_t)wave * 1024u;
+    wlast = wbase - (((PW - 1) * NW + wave >= K::NINST) ? (uint32_t)NW * 1024u : 0u);
 #pragma unroll
     for (int j = 0; j < PW; ++j) {
-      const int i = j * NW + wave;
-      rel[j] = i < K::NINST ? K::rel_offset(i, lane) : 0u;
+      int f = j * NW + wave;
+      if (f >= K::NINST) f -= NW;
+      rel[j] = K::rel_offset(f, lane);
     }
   }
-  __device__ __forceinline__ void k(__amdgpu_buffer_rsrc_t r, u16* dst, uint32_t tile_byte, int j,
-                                    int wave) const {
-    const int i = j * NW + wave;
-    if (i < K::NINST) K::issue_full(r, dst, tile_byte, i, rel[j]);
+  // Load n (a constant once the caller's loop is unrolled) of the tile whose
+  // first byte is kbyte into the tile at LDS byte address tile.
+  template <int J = 0>
+  __device__ __forceinline__ void issue_n(int n, uint32_t tile, u32x4 rK, uint32_t kbyte) const {
+    if constexpr (J < PW) {
+      if (n == J) dma16<J * NW * 1024>(rK, tile + (J == PW - 1 ? wlast : wbase), rel[J], kbyte);
+      else issue_n<J + 1>(n, tile, rK, kbyte);
+    }
   }
 };
 

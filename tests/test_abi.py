@@ -65,17 +65,30 @@ FAKE = ctypes.c_void_p(0x10000)     # aligned, never dereferenced: validation fa
 ])
 def test_dense_rejects_bad_problems(lib, kw, status):
     p = _prob(**kw)
-    assert lib.adaspa_dense_attn_lse(ctypes.byref(p), FAKE, FAKE, FAKE, FAKE, None, None) == status
+    assert lib.adaspa_dense_attn_lse(ctypes.byref(p), FAKE, FAKE, FAKE, FAKE, None, None, 0, None) == status
+    assert lib.adaspa_dense_attn_workspace(ctypes.byref(p)) == 0
 
 
 def test_dense_rejects_null_and_misaligned(lib):
     p = _prob()
-    assert lib.adaspa_dense_attn_lse(None, FAKE, FAKE, FAKE, FAKE, None, None) == 1
-    assert lib.adaspa_dense_attn_lse(ctypes.byref(p), None, FAKE, FAKE, FAKE, None, None) == 1
+    assert lib.adaspa_dense_attn_lse(None, FAKE, FAKE, FAKE, FAKE, None, None, 0, None) == 1
+    assert lib.adaspa_dense_attn_lse(ctypes.byref(p), None, FAKE, FAKE, FAKE, None, None, 0, None) == 1
     assert lib.adaspa_dense_attn_lse(ctypes.byref(p), ctypes.c_void_p(0x10008), FAKE, FAKE, FAKE,
-                                     None, None) == 1
+                                     None, None, 0, None) == 1
     assert lib.adaspa_dense_attn_lse(ctypes.byref(p), FAKE, FAKE, FAKE, FAKE,
-                                     ctypes.c_void_p(0x10002), None) == 1
+                                     ctypes.c_void_p(0x10002), None, 0, None) == 1
+
+
+def test_dense_workspace_checks(lib):
+    """The work-queue workspace is optional; when given it must be large
+    enough and 16-byte aligned (checked before anything is enqueued)."""
+    p = _prob()
+    need = lib.adaspa_dense_attn_workspace(ctypes.byref(p))
+    assert need >= 32 and need % 16 == 0
+    assert lib.adaspa_dense_attn_lse(ctypes.byref(p), FAKE, FAKE, FAKE, FAKE, None, FAKE,
+                                     need - 1, None) == 4
+    assert lib.adaspa_dense_attn_lse(ctypes.byref(p), FAKE, FAKE, FAKE, FAKE, None,
+                                     ctypes.c_void_p(0x10004), need, None) == 4
 
 
 def test_capacity_and_workspace(lib):

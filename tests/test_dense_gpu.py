@@ -76,6 +76,21 @@ def test_dense_deterministic_and_lse_optional():
     assert torch.equal(o1, o2) and torch.equal(l1, l2) and torch.equal(o1, o3)
 
 
+def test_dense_work_queue_matches_static_split():
+    """The per-XCD work queues only change which CU computes a tile: the
+    output and LSE are bitwise those of the static split, for a tile count
+    that does not divide by the eight queues, and on back-to-back calls that
+    reuse one workspace (the counters are cleared by each call)."""
+    w = TINY.replace(head_dim=128, heads=3, seqlen=1900, patches=459)
+    q, k, v = make_qkv(w, device="cuda")
+    o0, l0 = ad.dense_attn_lse(q, k, v, balance=False)
+    ws = torch.empty(ad.dense_attn_workspace(q.shape), dtype=torch.uint8, device="cuda")
+    for _ in range(3):
+        o1, l1 = ad.dense_attn_lse(q, k, v, workspace=ws)
+        torch.cuda.synchronize()
+        assert torch.equal(o0, o1) and torch.equal(l0, l1)
+
+
 def test_dense_batch_and_custom_scale():
     w = TINY.replace(batch=2, seqlen=512, text_len=64, patches=112)
     q, k, v = make_qkv(w, device="cuda")
