@@ -76,7 +76,7 @@ adaspa_status check_select(const adaspa_problem* p, const adaspa_select* s) {
 }
 
 struct WsLayout {
-  size_t idx, prefix, curve, headk, base, total;
+  size_t idx, prefix, curve, headk, base, claim, total;
 };
 
 WsLayout workspace_layout(const adaspa_problem* p) {
@@ -90,6 +90,7 @@ WsLayout workspace_layout(const adaspa_problem* p) {
   w.curve = off;  off = align_up(off + bh * nb * sizeof(int64_t));
   w.headk = off;  off = align_up(off + bh * sizeof(int32_t));
   w.base = off;   off = align_up(off + bh * sizeof(int64_t));
+  w.claim = off;  off = align_up(off + 8 * sizeof(uint32_t));   // mass-pass work queues
   w.total = off;
   return w;
 }
@@ -250,6 +251,7 @@ adaspa_status adaspa_block_search(const adaspa_problem* prob, const void* q, con
     m.nkb = nb;
     m.scale_log2 = scale_of(prob) * 1.4426950408889634f;
     m.xcd_map = xcd_map_mode(1);
+    m.claim = (uint32_t*)((char*)workspace + wl.claim);
     if (launch_block_mass(m, prob->head_dim, s) != hipSuccess) return ADASPA_ERR_HIP;
   }
 

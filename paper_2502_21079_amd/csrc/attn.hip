@@ -712,6 +712,15 @@ __global__ __launch_bounds__(256, 2) void block_mass_kernel(MassParams a) {
   int bh, pg;
   if (a.xcd_map == 2) {
     xcd_chunk_map(blockIdx.x, ngrp, a.batch_heads, bh, pg);
+  } else if (a.claim != nullptr) {           // per-XCD work queues (see claim_item)
+    __shared__ int s_item;
+    if (threadIdx.x == 0) s_item = claim_item(a.claim, a.n_items);
+    __syncthreads();
+    const int item = s_item;
+    if (item < 0) return;
+    const int lid = a.xcd_map ? xcd_remap(item, a.n_items) : item;
+    bh = lid / ngrp;
+    pg = lid % ngrp;
   } else {
     const int lid = a.xcd_map ? xcd_remap(blockIdx.x, a.n_wg) : (int)blockIdx.x;
     bh = lid / ngrp;
@@ -904,7 +913,14 @@ hipError_t launch_sparse(AttnParams a, int D, hipStream_t st) {
 
 template <int D, int QB>
 static hipError_t launch_mass_t(MassParams a, hipStream_t st) {
-  a.n_wg = (a.nkb + QB - 1) / QB * a.batch_heads;
+  a.n_items = (a.nkb + QB - 1) / QB * a.batch_heads;
+  a.n_wg = a.n_items;
+  if (a.claim != nullptr) {                  // as in launch_dense
+    a.n_wg = a.n_items + (a.n_items + 3) / 4;
+    hipLaunchKernelGGL(claim_reset_kernel, dim3(1), dim3(64), 0, st, a.claim);
+    const hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+  }
   hipLaunchKernelGGL((block_mass_kernel<D, QB>), dim3(a.n_wg), dim3(256), 0, st, a);
   return hipGetLastError();
 }

@@ -44,6 +44,8 @@ struct MassParams {
   int n_wg;
   float scale_log2;
   int xcd_map;
+  uint32_t* claim;            // 8 work-queue counters (one per XCD), or null
+  int n_items;                // with claim: work items (head, query-block group)
 };
 
 constexpr int kMaxHeads = 512;
