@@ -327,7 +327,10 @@ def main():
               **txt)
         return res
 
-    # pattern for a sparse-only profile run
+    # the fresh LSE for a search-only profile run, and the pattern for a
+    # sparse-only one
+    if args.kernel == "search":
+        ad.dense_attn_lse(q, k, v, out=out, lse=lse)
     if args.kernel == "sparse":
         ad.dense_attn_lse(q, k, v, out=out, lse=lse)
         if args.sparse_keep > 0:
