@@ -387,10 +387,20 @@ def main():
         mix_rng = np.random.default_rng(3)
         mix = [int(x) for x in mix_rng.integers(500, 5001, size=H)]
         for name, params in [("keep5", [500] * H), ("keep10", [1000] * H), ("keep20", [2000] * H),
-                             ("keep50", [5000] * H), ("mix5to50", mix)]:
-            r = ad.block_search(None, None, None, block=blk, text_start=w.text_start,
-                                text_len=w.text_len, mode="topk", head_param_bp=params,
-                                scores=res.block_mass, shape=(B, H, L, D))
+                             ("keep50", [5000] * H), ("mix5to50", mix), ("hierarchical_s90", None)]:
+            if params is None:
+                # the paper's head-adaptive rule (Sec. 4.2): base sparsity 0.9,
+                # heads with Recall above 0.8 move to (1+s)/2, as many of the
+                # lowest to (3s-1)/2
+                sel_ms = Timer()
+                r = sel_ms("sel", ad.block_search, None, None, None, block=blk, text_start=w.text_start,
+                           text_len=w.text_len, mode="hierarchical", base_sparsity_bp=9000,
+                           recall_threshold_bp=8000, scores=res.block_mass, shape=(B, H, L, D))
+                sel_time = float(np.mean(sel_ms.collect()["sel"]))
+            else:
+                r = ad.block_search(None, None, None, block=blk, text_start=w.text_start,
+                                    text_len=w.text_len, mode="topk", head_param_bp=params,
+                                    scores=res.block_mass, shape=(B, H, L, D))
             tm = Timer()
             for _ in range(2):
                 ad.block_sparse_attn(q, k, v, r.row_ptr, r.col_idx, block=blk, out=sp_out, want_lse=False,
@@ -406,6 +416,10 @@ def main():
                            "density": round(nz / (B * H * nb * nb), 4),
                            "speedup_vs_dense": round(dense_ms / ms, 3),
                            "head_imbalance": round(float(hk.max() / hk.mean()), 3)}
+            if params is None:
+                sweep[name].update({"selection_ms": round(sel_time, 3),
+                                    "head_k": [int(x) for x in hk],
+                                    "head_recall_mean": round(float(r.head_recall.float().mean().item()), 4)})
 
     amort = None
     if not args.no_amortised and not args.no_sweep:
