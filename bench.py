@@ -416,6 +416,25 @@ def main():
                            "density": round(nz / (B * H * nb * nb), 4),
                            "speedup_vs_dense": round(dense_ms / ms, 3),
                            "head_imbalance": round(float(hk.max() / hk.mean()), 3)}
+            if name == "mix5to50":
+                # the same total of kept blocks at one count for every head
+                # (the keep fraction of the mix's density): isolates what the
+                # head imbalance costs
+                u_bp = int(round(10000 * nz / (B * H * nb * nb)))
+                ru = ad.block_search(None, None, None, block=blk, text_start=w.text_start,
+                                     text_len=w.text_len, mode="topk", head_param_bp=[u_bp] * H,
+                                     scores=res.block_mass, shape=(B, H, L, D))
+                tu = Timer()
+                for _ in range(2):
+                    ad.block_sparse_attn(q, k, v, ru.row_ptr, ru.col_idx, block=blk, out=sp_out,
+                                         want_lse=False, **txt)
+                for _ in range(max(3, args.steps)):
+                    tu("s", ad.block_sparse_attn, q, k, v, ru.row_ptr, ru.col_idx, block=blk,
+                       out=sp_out, want_lse=False, **txt)
+                ms_u = float(np.mean(tu.collect()["s"]))
+                sweep[name].update({"uniform_same_nnz": {"keep_bp": u_bp, "nnz_ratio": round(ru.nnz() / nz, 4),
+                                                         "ms": round(ms_u, 3)},
+                                    "ms_vs_uniform_same_nnz": round(ms / ms_u * nz / ru.nnz(), 4)})
             if params is None:
                 sweep[name].update({"selection_ms": round(sel_time, 3),
                                     "head_k": [int(x) for x in hk],
