@@ -240,11 +240,13 @@ __global__ __launch_bounds__(64 * NW, NW >= 8 ? 1 : 2) void attn_fwd_kernel(Attn
       asm volatile("" : "+s"(fill));
       const uint32_t mbyte = ld.mixed_v ? vbyte : kbyte;
       auto loads = [&](int slot) {
-        // Load n goes to slot n * NM / PW (at most one per slot).
-        constexpr int PW = LD::PW, NM = 2 * NK + 4 * ND;
-        static_assert(PW <= NM, "one load instruction per slot at most");
-        const int n = (slot * PW + NM - 1) / NM;
-        if (n >= PW || (n * NM) / PW != slot) return;
+        // Load n goes to slot n * SPAN / PW (at most one per slot): the
+        // loads fill the first 5/16 of the step, so the last of them has
+        // most of the step to land before the wait at its end.
+        constexpr int PW = LD::PW, SPAN = (2 * NK + 4 * ND) * 5 / 16;
+        static_assert(PW <= SPAN, "one load instruction per slot at most");
+        const int n = (slot * PW + SPAN - 1) / SPAN;
+        if (n >= PW || (n * SPAN) / PW != slot) return;
         ld.issue_n(n, fill, rKw, rVw, rMw, kbyte, vbyte, mbyte);
       };
       f32x16 s_next[2];
@@ -573,10 +575,10 @@ __global__ __launch_bounds__(64 * NW, NW >= 8 ? 1 : 2) void attn_sparse_pair_ker
       asm volatile("" : "+s"(fill));
       const uint32_t mbyte = ld.mixed_v ? vbyte : kbyte;
       auto loads = [&](int slot) {
-        constexpr int PW = LD::PW, NM = 2 * NK + 4 * ND;
-        static_assert(PW <= NM, "one load instruction per slot at most");
-        const int n = (slot * PW + NM - 1) / NM;
-        if (n >= PW || (n * NM) / PW != slot) return;
+        constexpr int PW = LD::PW, SPAN = (2 * NK + 4 * ND) * 5 / 16;   // as in attn_fwd_kernel
+        static_assert(PW <= SPAN, "one load instruction per slot at most");
+        const int n = (slot * PW + SPAN - 1) / SPAN;
+        if (n >= PW || (n * SPAN) / PW != slot) return;
         ld.issue_n(n, fill, rKw, rVw, rMw, kbyte, vbyte, mbyte);
       };
       f32x16 s_next[2];
