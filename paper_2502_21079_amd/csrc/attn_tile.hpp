@@ -433,21 +433,38 @@ __device__ __forceinline__ void pipelined_step(Hook&& hook, const u16* klane, co
     }
   };
 
+  // Slot i owns scores e in [i*PER, (i+1)*PER) of the tile's 32, in (group,
+  // element) order.  Their softmax is pipelined over three slots: slot i
+  // forms the exponent arguments, slot i+1 takes the exponentials, slot i+2
+  // rounds each completed pair to bf16 and adds it to the row sum, so no
+  // instruction waits on the result of the one just before it.  The last
+  // two slots' shares are finished after the MFMAs.
+  constexpr int PER = 32 / NM;
   const bf16x2 ones = {(__bf16)1.0f, (__bf16)1.0f};
-  float ts = 0.f, x0 = 0.f;
-  auto valu = [&](int i) {
-    // scores e in [i*32/NM, (i+1)*32/NM) of the tile's 32, in (group,
-    // element) order; a pair is rounded to bf16 and summed once complete.
-    constexpr int PER = 32 / NM;
+  float ts = 0.f;
+  float arg[32], ex[32];
+  auto stage_arg = [&](int i) {
+#pragma unroll
+    for (int u = 0; u < PER; ++u) {
+      const int e = i * PER + u;
+      arg[e] = fmaf(s_cur[e >> 4][e & 15], sl2, -mc);
+      pin(arg[e]);
+    }
+  };
+  auto stage_exp = [&](int i) {
+#pragma unroll
+    for (int u = 0; u < PER; ++u) {
+      const int e = i * PER + u;
+      ex[e] = fast_exp2(arg[e]);
+      pin(ex[e]);
+    }
+  };
+  auto stage_sum = [&](int i) {
 #pragma unroll
     for (int u = 0; u < PER; ++u) {
       const int e = i * PER + u, g = e >> 4, r = e & 15;
-      const float x = fast_exp2(fmaf(s_cur[g][r], sl2, -mc));
-      if ((e & 1) == 0) {
-        x0 = x;
-        pin(x0);
-      } else {
-        const bf16x2 pr = {(__bf16)x0, (__bf16)x};
+      if (e & 1) {
+        const bf16x2 pr = {(__bf16)ex[e - 1], (__bf16)ex[e]};
         p_cur[g][r >> 3][(r & 7) - 1] = pr[0];
         p_cur[g][r >> 3][r & 7] = pr[1];
         ts = __builtin_amdgcn_fdot2_f32_bf16(pr, ones, ts, false);
@@ -463,9 +480,14 @@ __device__ __forceinline__ void pipelined_step(Hook&& hook, const u16* klane, co
     if (i + LA < NM) fetch(i + LA);
     mfma(i);
     hook(i);
-    valu(i);
+    stage_arg(i);
+    if (i >= 1) stage_exp(i - 1);
+    if (i >= 2) stage_sum(i - 2);
     __builtin_amdgcn_sched_barrier(0);
   }
+  stage_exp(NM - 1);
+  stage_sum(NM - 2);
+  stage_sum(NM - 1);
   tsum = ts;
 }
 
@@ -488,10 +510,30 @@ __device__ __forceinline__ void mass_step(Hook&& hook, const u16* klane, const b
     if (ks == 0) s_next[g] = mfma32(op[j], qf[ks], f32x16{});
     else s_next[g] = mfma32(op[j], qf[ks], s_next[g]);
   };
-  auto valu = [&](int j) {
-    const int e0 = j * 32 / NM, e1 = (j + 1) * 32 / NM;
+  // Slot j owns scores [j*PER, (j+1)*PER); as in pipelined_step, slot j forms
+  // their exponent arguments, slot j+1 the exponentials and slot j+2 adds
+  // them to acc (in score order), the last two shares after the MFMAs.
+  constexpr int PER = 32 / NM;
+  float arg[32], ex[32];
+  auto stage_arg = [&](int j) {
 #pragma unroll
-    for (int e = e0; e < e1; ++e) acc += fast_exp2(fmaf(s_cur[e >> 4][e & 15], sl2, nlse2));
+    for (int u = 0; u < PER; ++u) {
+      const int e = j * PER + u;
+      arg[e] = fmaf(s_cur[e >> 4][e & 15], sl2, nlse2);
+      pin(arg[e]);
+    }
+  };
+  auto stage_exp = [&](int j) {
+#pragma unroll
+    for (int u = 0; u < PER; ++u) {
+      const int e = j * PER + u;
+      ex[e] = fast_exp2(arg[e]);
+      pin(ex[e]);
+    }
+  };
+  auto stage_sum = [&](int j) {
+#pragma unroll
+    for (int u = 0; u < PER; ++u) acc += ex[j * PER + u];
     pin(acc);
   };
 #pragma unroll
@@ -501,9 +543,14 @@ __device__ __forceinline__ void mass_step(Hook&& hook, const u16* klane, const b
     if (i + LA < NM) fetch(i + LA);
     mfma(i);
     hook(i);
-    valu(i);
+    stage_arg(i);
+    if (i >= 1) stage_exp(i - 1);
+    if (i >= 2) stage_sum(i - 2);
     __builtin_amdgcn_sched_barrier(0);
   }
+  stage_exp(NM - 1);
+  stage_sum(NM - 2);
+  stage_sum(NM - 1);
 }
 
 }  // namespace adaspa
