@@ -288,8 +288,11 @@ __device__ __forceinline__ void zero_lds(u16* p, int tid, int nt) {
 // Online softmax against a lazy reference.  Probabilities of a row are taken
 // as exp2(s * sl2 - mc) with mc = m * sl2 for a reference m (raw score units)
 // that is NOT the running maximum: it moves only when the probabilities of a
-// tile, summed over one lane's keys, exceed kTileSumLimit (or are positive at
-// all while m is still -inf), so no per-tile maximum is computed.  Every
+// tile, summed over one lane's keys, exceed kTileSumLimit, and on every tile
+// while m is still -inf (the first tile with a finite score sets it to that
+// tile's maximum, however negative: against mc = 0 a row whose scaled scores
+// all lie below the fp32 exponent range would otherwise sum to zero and never
+// set it), so no per-tile maximum is computed on the common path.  Every
 // probability then stays below 2^16 (no overflow of the fp32 sums), and the
 // final normalisation uses the same reference, so the result is the softmax
 // whatever the reference.  When the reference moves, sums taken against the
@@ -299,7 +302,7 @@ constexpr float kTileSumLimit = 65536.f;
 struct RowRef {
   float m = -INFINITY;   // reference, raw score units; -inf until a finite score is seen
   float mc = 0.f;        // m * sl2 (0 while m is -inf)
-  float lim = 0.f;       // tile sum above which the reference must move
+  float lim = -1.f;      // tile sum above which the reference must move (below any sum while m is -inf)
 
   // m <- max(m, row maximum of s) for the rows of this wave (the two
   // half-waves holding a row agree); returns the rescale factor of sums
@@ -317,7 +320,7 @@ struct RowRef {
     const float a = (mnew == -INFINITY) ? 1.f : fast_exp2((m - mnew) * sl2);
     m = mnew;
     mc = (m == -INFINITY) ? 0.f : m * sl2;
-    lim = (m == -INFINITY) ? 0.f : kTileSumLimit;
+    lim = (m == -INFINITY) ? -1.f : kTileSumLimit;
     return a;
   }
 };

@@ -184,3 +184,39 @@ def random_block_lists(nrows: int, nblocks: int, k: int, seed: int,
     row_ptr[1:] = torch.tensor([len(c) for c in cols], dtype=torch.int64).cumsum(0).to(torch.int32)
     col_idx = torch.tensor([c for row in cols for c in row], dtype=torch.int32)
     return row_ptr, col_idx
+
+
+EXTREME_KINDS = ("negative", "rising", "spiky")
+
+
+def make_extreme_qkv(kind: str, heads: int, seqlen: int, head_dim: int, seed: int = 11,
+                     device="cpu"):
+    """Seeded [1, H, L, D] bf16 inputs whose attention scores stress the
+    softmax bookkeeping.  Each kind comes with the softmax scale it is meant
+    for (returned second):
+
+    - ``negative``: q ~ -2 + 0.3 N, k ~ 2 + 0.3 N, scale 1, so every scaled
+      score of every row lies near -4 D, far below the fp32 exponent range;
+    - ``rising``: q ~ 2 + 0.3 N, key j ~ a j + 0.3 N, default scale 1/sqrt(D),
+      with a set so the scores rise by about 20 per 64 keys (the row maximum
+      moves on every tile, by far more than a tile's probabilities allow);
+    - ``spiky``: q, k ~ 2 N, scale 1, so scores spread by about 4 sqrt(D)
+      times their own scale: large, random jumps of the row maximum.
+
+    V is N(0, 1) throughout."""
+    assert kind in EXTREME_KINDS
+    H, L, D = heads, seqlen, head_dim
+    g = _gen(seed, 5150 + EXTREME_KINDS.index(kind), device)
+    nq = torch.randn(1, H, L, D, generator=g, device=device)
+    nk = torch.randn(1, H, L, D, generator=g, device=device)
+    v = torch.randn(1, H, L, D, generator=g, device=device)
+    if kind == "negative":
+        q, k, scale = -2.0 + 0.3 * nq, 2.0 + 0.3 * nk, 1.0
+    elif kind == "rising":
+        a = 20.0 / (64 * 2.0 * D ** 0.5)
+        j = torch.arange(L, device=device, dtype=torch.float32).view(1, 1, L, 1)
+        q, k, scale = 2.0 + 0.3 * nq, a * j + 0.3 * nk, D ** -0.5
+    else:
+        q, k, scale = 2.0 * nq, 2.0 * nk, 1.0
+    bf = torch.bfloat16
+    return (q.to(bf).contiguous(), k.to(bf).contiguous(), v.to(bf).contiguous()), scale
