@@ -10,7 +10,7 @@ import torch
 import oracle
 import paper_2502_21079_amd as ad
 from workloads import EXTREME_KINDS, make_extreme_qkv, random_block_lists
-from _helpers import check_lse, check_out, f64
+from _helpers import check_lse, check_mass, check_out, f64
 
 pytestmark = pytest.mark.gpu
 
@@ -56,3 +56,22 @@ def test_all_blocks_equals_dense_extreme(kind, block):
     os_, ls = ad.block_sparse_attn(q, k, v, rp, ci, block=block, scale=scale, text_start=0, text_len=0)
     torch.cuda.synchronize()
     assert torch.equal(od, os_) and torch.equal(ld, ls)
+
+
+@pytest.mark.parametrize("kind", EXTREME_KINDS)
+@pytest.mark.parametrize("D,block,L", [(64, 64, 1000), (128, 128, 777)])
+def test_mass_extreme_scores(kind, D, block, L):
+    """The mass pass with the oracle's fp32 LSE on both sides: exp(s - LSE)
+    summed per block stays exact where the scores span hundreds of units."""
+    (q, k, v), scale = make_extreme_qkv(kind, heads=2, seqlen=L, head_dim=D, device="cuda")
+    lse = torch.empty(1, 2, L, dtype=torch.float32)
+    for h in range(2):
+        _, l_ref = oracle.dense_attention(f64(q[0, h]), f64(k[0, h]), f64(v[0, h]), scale)
+        lse[0, h] = torch.from_numpy(l_ref.astype(np.float32))
+    lse = lse.cuda()
+    res = ad.block_search(q, k, lse, block=block, text_start=0, text_len=0, mode="topk",
+                          head_param_bp=[5000, 5000], scale=scale)
+    torch.cuda.synchronize()
+    for h in range(2):
+        ref = oracle.block_mass(f64(q[0, h]), f64(k[0, h]), f64(lse[0, h]), scale, block)
+        check_mass(res.block_mass[0, h], ref, f"{kind} h{h}")
