@@ -171,6 +171,10 @@ adaspa_status adaspa_block_search(const adaspa_problem* prob, const void* q,
                                   float* head_recall, void* workspace,
                                   size_t workspace_bytes, void* stream);
 
+/* Device bytes of the optional workspace of adaspa_block_sparse_attn (0 for
+ * invalid arguments). */
+size_t adaspa_block_sparse_attn_workspace(const adaspa_problem* prob);
+
 /* Blockified sparse attention (Sec. 4.1, bias -c(1-M) with c -> inf).
  *   out[b,h,i,:] = sum_{j in kept(p(i))} exp(scale*q_i.k_j - lseM_i) v_j
  *   lseM[b,h,i]  = log sum_{j in kept(p(i))} exp(scale * q_i . k_j)
@@ -183,12 +187,21 @@ adaspa_status adaspa_block_search(const adaspa_problem* prob, const void* q,
  * patterns never read out of bounds.  Rows should be strictly ascending
  * (a repeated block would be counted twice).  prob->text_start/text_len only
  * order the work (the text query blocks, which keep every key block under the
- * text sink, are started first); the results do not depend on them. */
+ * text sink, are started first); the results do not depend on them.
+ * workspace (optional, caller-owned, 16-byte aligned, at least
+ * adaspa_block_sparse_attn_workspace() bytes, contents need not be
+ * initialised) holds per-XCD work-queue counters: the last tenth of the query
+ * blocks then goes to the XCDs that run ahead; with NULL all work is split
+ * statically.  The results are bitwise the same either way.  The call clears
+ * the counters itself (with a kernel on `stream`); calls that may run
+ * concurrently need separate workspaces.  ADASPA_ERR_WORKSPACE if it is too
+ * small or misaligned. */
 adaspa_status adaspa_block_sparse_attn(const adaspa_problem* prob, const void* q,
                                        const void* k, const void* v,
                                        const int32_t* row_ptr,
                                        const int32_t* col_idx, int64_t col_count,
-                                       void* out, float* lse_out, void* stream);
+                                       void* out, float* lse_out, void* workspace,
+                                       size_t workspace_bytes, void* stream);
 
 #ifdef __cplusplus
 }

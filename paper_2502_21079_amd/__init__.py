@@ -22,7 +22,8 @@ from typing import Optional, Sequence
 
 import torch
 
-__all__ = ["dense_attn_lse", "dense_attn_workspace", "block_search", "block_sparse_attn", "SearchResult",
+__all__ = ["dense_attn_lse", "dense_attn_workspace", "block_search", "block_sparse_attn",
+           "block_sparse_attn_workspace", "SearchResult",
            "library_path", "load_library", "AdaspaError", "EXPORTED_SYMBOLS",
            "block_search_workspace", "block_search_capacity"]
 
@@ -31,7 +32,8 @@ _LIB_NAME = "libadaspa.so"
 
 EXPORTED_SYMBOLS = ("adaspa_status_string", "adaspa_dense_attn_workspace", "adaspa_dense_attn_lse",
                     "adaspa_block_search_workspace", "adaspa_block_search_capacity",
-                    "adaspa_block_search", "adaspa_block_sparse_attn")
+                    "adaspa_block_search", "adaspa_block_sparse_attn_workspace",
+                    "adaspa_block_sparse_attn")
 
 SELECT_TOPK = 0
 SELECT_COVERAGE = 1
@@ -89,9 +91,11 @@ def load_library():
     lib.adaspa_block_search.restype = ctypes.c_int
     lib.adaspa_block_search.argtypes = [P, vp, vp, f32p, S, f32p, i32p, i32p, ctypes.c_int64,
                                         i32p, f32p, vp, ctypes.c_size_t, vp]
+    lib.adaspa_block_sparse_attn_workspace.restype = ctypes.c_size_t
+    lib.adaspa_block_sparse_attn_workspace.argtypes = [P]
     lib.adaspa_block_sparse_attn.restype = ctypes.c_int
     lib.adaspa_block_sparse_attn.argtypes = [P, vp, vp, vp, i32p, i32p, ctypes.c_int64, vp,
-                                             f32p, vp]
+                                             f32p, vp, ctypes.c_size_t, vp]
     _lib = lib
     return lib
 
@@ -261,9 +265,15 @@ def block_search(q, k, lse, *, block: int, text_start: int, text_len: int,
 
 def block_sparse_attn(q, k, v, row_ptr, col_idx, *, block: int, scale: Optional[float] = None,
                       out=None, lse=None, want_lse: bool = True, text_start: int = 0,
-                      text_len: int = 0):
+                      text_len: int = 0, workspace=None, balance: bool = True):
     """Blockified sparse attention over the CSR key-block lists.  Returns (out, lse).
-    ``text_start``/``text_len`` only order the work (text query blocks first)."""
+    ``text_start``/``text_len`` only order the work (text query blocks first).
+    With ``balance`` (the default) the last tenth of the query blocks goes to
+    the XCDs that run ahead, through per-XCD work queues whose counters live
+    in ``workspace`` (uint8 CUDA tensor of at least
+    ``block_sparse_attn_workspace(q.shape, block)`` bytes; allocated here when
+    not given); ``balance=False`` splits the work statically.  The results
+    are the same either way."""
     _check_qkv(q, k, v)
     lib = load_library()
     B, H, L, D = q.shape
@@ -278,7 +288,23 @@ def block_sparse_attn(q, k, v, row_ptr, col_idx, *, block: int, scale: Optional[
     if lse is None and want_lse:
         lse = torch.empty(B, H, L, dtype=torch.float32, device=q.device)
     prob = _problem(q, block, text_start, text_len, scale)
+    ws_bytes = 0
+    if balance:
+        ws_bytes = int(lib.adaspa_block_sparse_attn_workspace(ctypes.byref(prob)))
+        if workspace is None:
+            workspace = torch.empty(ws_bytes, dtype=torch.uint8, device=q.device)
+        ws_bytes = workspace.numel() * workspace.element_size()
+    else:
+        workspace = None
     _check(lib.adaspa_block_sparse_attn(ctypes.byref(prob), _ptr(q), _ptr(k), _ptr(v),
                                         _ptr(row_ptr), _ptr(col_idx), int(col_idx.numel()),
-                                        _ptr(out), _ptr(lse), _stream(q.device)))
+                                        _ptr(out), _ptr(lse), _ptr(workspace),
+                                        ctypes.c_size_t(ws_bytes), _stream(q.device)))
     return out, lse
+
+
+def block_sparse_attn_workspace(shape, block: int = 128, scale: Optional[float] = None) -> int:
+    """Bytes of the work-queue workspace of :func:`block_sparse_attn`."""
+    B, H, L, D = shape
+    prob = _Problem(B, H, L, D, block, 0, 0, 0.0 if scale is None else float(scale))
+    return int(load_library().adaspa_block_sparse_attn_workspace(ctypes.byref(prob)))

@@ -152,7 +152,12 @@ const char* adaspa_status_string(adaspa_status s) {
 
 size_t adaspa_dense_attn_workspace(const adaspa_problem* prob) {
   if (check_problem(prob) != ADASPA_OK) return 0;
-  return kAlign;   // eight 32-bit work-queue counters, padded
+  return kAlign;   // nine 32-bit work-queue counters, padded
+}
+
+size_t adaspa_block_sparse_attn_workspace(const adaspa_problem* prob) {
+  if (check_problem(prob) != ADASPA_OK) return 0;
+  return kAlign;   // as for dense attention
 }
 
 adaspa_status adaspa_dense_attn_lse(const adaspa_problem* prob, const void* q, const void* k,
@@ -291,7 +296,8 @@ adaspa_status adaspa_block_search(const adaspa_problem* prob, const void* q, con
 adaspa_status adaspa_block_sparse_attn(const adaspa_problem* prob, const void* q, const void* k,
                                        const void* v, const int32_t* row_ptr,
                                        const int32_t* col_idx, int64_t col_count, void* out,
-                                       float* lse_out, void* stream) {
+                                       float* lse_out, void* workspace, size_t workspace_bytes,
+                                       void* stream) {
   adaspa_status st = check_problem(prob);
   if (st != ADASPA_OK) return st;
   if (!q || !k || !v || !out || !row_ptr || (!col_idx && col_count > 0) || col_count < 0)
@@ -300,6 +306,8 @@ adaspa_status adaspa_block_sparse_attn(const adaspa_problem* prob, const void* q
       (lse_out && ((uintptr_t)lse_out & 3u)) || ((uintptr_t)row_ptr & 3u) ||
       ((uintptr_t)col_idx & 3u))
     return ADASPA_ERR_INVALID_ARG;
+  if (workspace && (workspace_bytes < adaspa_block_sparse_attn_workspace(prob) || !aligned16(workspace)))
+    return ADASPA_ERR_WORKSPACE;
   AttnParams a;
   memset(&a, 0, sizeof a);
   a.q = (const u16*)q;
@@ -317,6 +325,7 @@ adaspa_status adaspa_block_sparse_attn(const adaspa_problem* prob, const void* q
   a.scale = scale_of(prob);
   a.scale_log2 = a.scale * 1.4426950408889634f;
   a.xcd_map = xcd_map_mode(3);
+  a.claim = (uint32_t*)workspace;
   // Text query blocks keep every key block under the text sink, so they are
   // the longest rows; the kernel starts them first (the result does not
   // depend on the order).

@@ -18,24 +18,33 @@ namespace adaspa {
 // empty, the next item of another queue, and exits when all are empty.  The
 // grid has more workgroups than items, so a faster XCD simply runs more of
 // them.  Items keep their order within a queue, so neighbouring tiles still
-// share an L2.
+// share an L2.  Block-sparse attention runs the first nine tenths of its
+// items in the static order and queues only the rest: on its short rows the
+// claim's round trip would otherwise sit in every workgroup's prologue.
 __device__ __forceinline__ int xcc_id() {
   return __builtin_amdgcn_s_getreg(20 | (0 << 6) | (3 << 11)) & 7;   // HW_REG_XCC_ID[3:0]
 }
 
-__device__ __forceinline__ int claim_item(uint32_t* ctr, int n) {
+// Takes an item of [n0, n) (n0 a multiple of 8, so item n0 + y + 8j is in
+// queue y), or returns -1 when every queue is empty.  With FLAG, ctr[8] is
+// set once a workgroup has found all queues empty, and later workgroups
+// return after reading it instead of trying all eight counters.
+template <bool FLAG = false>
+__device__ __forceinline__ int claim_item(uint32_t* ctr, int n0, int n) {
+  if (FLAG && __atomic_load_n(&ctr[8], __ATOMIC_RELAXED) != 0u) return -1;
   const int x = xcc_id();
   for (int k = 0; k < 8; ++k) {
     const int y = (x + k) & 7;
-    const int m = (n - y + 7) / 8;            // items of queue y
+    const int m = (n - n0 - y + 7) / 8;       // items of queue y
     const unsigned j = atomicAdd(&ctr[y], 1u);
-    if ((int)j < m) return (int)j * 8 + y;
+    if ((int)j < m) return n0 + (int)j * 8 + y;
   }
+  if (FLAG) atomicExch(&ctr[8], 1u);
   return -1;
 }
 
 __global__ void claim_reset_kernel(uint32_t* ctr) {
-  if (threadIdx.x < 8) ctr[threadIdx.x] = 0u;
+  if (threadIdx.x < 9) ctr[threadIdx.x] = 0u;
 }
 
 // ---------------------------------------------------------------------------
@@ -72,10 +81,18 @@ __global__ __launch_bounds__(64 * NW, NW >= 8 ? 1 : 2) void attn_fwd_kernel(Attn
   if (a.xcd_map == 2) {
     xcd_chunk_map(blockIdx.x, a.nqt, a.batch_heads, bh, qt);
   } else if (SPARSE && (a.xcd_map == 1 || a.xcd_map == 3)) {
-    text_first_map(blockIdx.x, a.n_wg, a.nqt, a.tq0, a.tq1 - a.tq0, bh, qt, a.xcd_map == 3);
+    int item = (int)blockIdx.x;
+    if (item >= a.n_static) {                // the queued tail (see claim_item)
+      __shared__ int s_tail;
+      if (threadIdx.x == 0) s_tail = claim_item<true>(a.claim, a.n_static, a.n_items);
+      __syncthreads();
+      item = s_tail;
+      if (item < 0) return;
+    }
+    text_first_map(item, a.n_items, a.nqt, a.tq0, a.tq1 - a.tq0, bh, qt, a.xcd_map == 3);
   } else if (!SPARSE && a.claim != nullptr) {
     __shared__ int s_item;
-    if (threadIdx.x == 0) s_item = claim_item(a.claim, a.n_items);
+    if (threadIdx.x == 0) s_item = claim_item(a.claim, 0, a.n_items);
     __syncthreads();
     const int item = s_item;
     if (item < 0) return;                    // every item is taken
@@ -377,7 +394,15 @@ __global__ __launch_bounds__(64 * NW, NW >= 8 ? 1 : 2) void attn_sparse_pair_ker
 
   int bh, pq;
   if (a.xcd_map == 1 || a.xcd_map == 3) {
-    text_first_map(blockIdx.x, a.n_wg, a.nqt, a.tq0, a.tq1 - a.tq0, bh, pq, a.xcd_map == 3);
+    int item = (int)blockIdx.x;
+    if (item >= a.n_static) {                // as in attn_fwd_kernel
+      __shared__ int s_tail;
+      if (threadIdx.x == 0) s_tail = claim_item<true>(a.claim, a.n_static, a.n_items);
+      __syncthreads();
+      item = s_tail;
+      if (item < 0) return;
+    }
+    text_first_map(item, a.n_items, a.nqt, a.tq0, a.tq1 - a.tq0, bh, pq, a.xcd_map == 3);
   } else {
     const int lid = a.xcd_map ? xcd_remap(blockIdx.x, a.n_wg) : (int)blockIdx.x;
     bh = lid / a.nqt;
@@ -716,7 +741,7 @@ __global__ __launch_bounds__(256, 2) void block_mass_kernel(MassParams a) {
     xcd_chunk_map(blockIdx.x, ngrp, a.batch_heads, bh, pg);
   } else if (a.claim != nullptr) {           // per-XCD work queues (see claim_item)
     __shared__ int s_item;
-    if (threadIdx.x == 0) s_item = claim_item(a.claim, a.n_items);
+    if (threadIdx.x == 0) s_item = claim_item(a.claim, 0, a.n_items);
     __syncthreads();
     const int item = s_item;
     if (item < 0) return;
@@ -892,23 +917,41 @@ hipError_t launch_dense(AttnParams a, int D, hipStream_t st) {
   return launch_attn<128, 8, false>(a, st);
 }
 
+// Work items of block-sparse attention: with a workspace, the first nine
+// tenths (rounded down to a multiple of 8) in the static order and the rest
+// claimed from the per-XCD queues, with half as many extra workgroups as
+// queued items (a fast XCD takes up to that many more than its share); the
+// queues serve only the mappings that name items (1 and 3).
+static hipError_t plan_sparse_items(AttnParams& a, hipStream_t st) {
+  a.n_items = a.nqt * a.batch_heads;
+  a.n_static = a.n_items;
+  a.n_wg = a.n_items;
+  if (a.claim == nullptr || !(a.xcd_map == 1 || a.xcd_map == 3)) return hipSuccess;
+  a.n_static = (int)((int64_t)a.n_items * 9 / 10) / 8 * 8;
+  a.n_wg = a.n_items + (a.n_items - a.n_static) / 2;
+  hipLaunchKernelGGL(claim_reset_kernel, dim3(1), dim3(64), 0, st, a.claim);
+  return hipGetLastError();
+}
+
 hipError_t launch_sparse(AttnParams a, int D, hipStream_t st) {
   if (a.block == 64) {
     // One workgroup per pair of query blocks (128 rows); text ranges in pairs.
     a.nqt = (a.nkb + 1) / 2;
-    a.n_wg = a.nqt * a.batch_heads;
     if (a.tq1 > a.tq0) {
       a.tq0 = a.tq0 / 2;
       a.tq1 = (a.tq1 + 1) / 2;
       if (a.tq1 - a.tq0 >= a.nqt) a.tq0 = a.tq1 = 0;
     }
+    const hipError_t e = plan_sparse_items(a, st);
+    if (e != hipSuccess) return e;
     if (D == 64) hipLaunchKernelGGL((attn_sparse_pair_kernel<64, 4>), dim3(a.n_wg), dim3(256), 0, st, a);
     else hipLaunchKernelGGL((attn_sparse_pair_kernel<128, 4>), dim3(a.n_wg), dim3(256), 0, st, a);
     return hipGetLastError();
   }
   // One workgroup per query block of 128 (four waves).
   a.nqt = a.nkb;
-  a.n_wg = a.nkb * a.batch_heads;
+  const hipError_t e = plan_sparse_items(a, st);
+  if (e != hipSuccess) return e;
   if (D == 64) return launch_attn<64, 4, true>(a, st);
   return launch_attn<128, 4, true>(a, st);
 }

@@ -28,8 +28,9 @@ struct AttnParams {
   int xcd_map;                // 0 hardware order, 1 contiguous per XCD, 2 head-chunked,
                               // 3 sparse: text first, then head-chunked
   int tq0, tq1;               // sparse: text query blocks [tq0, tq1), dispatched first
-  uint32_t* claim;            // dense: 8 work-queue counters (one per XCD), or null
-  int n_items;                // dense with claim: work items (head, query tile)
+  uint32_t* claim;            // 9 work-queue counters (one per XCD + a flag), or null
+  int n_items;                // work items: (head, query tile) or (head, query block / pair)
+  int n_static;               // sparse: items [0, n_static) run in the static order
 };
 
 struct MassParams {

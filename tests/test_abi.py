@@ -84,7 +84,7 @@ def test_dense_workspace_checks(lib):
     enough and 16-byte aligned (checked before anything is enqueued)."""
     p = _prob()
     need = lib.adaspa_dense_attn_workspace(ctypes.byref(p))
-    assert need >= 32 and need % 16 == 0
+    assert need >= 36 and need % 16 == 0
     assert lib.adaspa_dense_attn_lse(ctypes.byref(p), FAKE, FAKE, FAKE, FAKE, None, FAKE,
                                      need - 1, None) == 4
     assert lib.adaspa_dense_attn_lse(ctypes.byref(p), FAKE, FAKE, FAKE, FAKE, None,
@@ -165,13 +165,26 @@ def test_search_rejects_bad_arguments(lib):
 def test_sparse_rejects_bad_arguments(lib):
     p = _prob()
     assert lib.adaspa_block_sparse_attn(ctypes.byref(p), FAKE, FAKE, FAKE, None, FAKE, 10, FAKE,
-                                        None, None) == 1
+                                        None, None, 0, None) == 1
     assert lib.adaspa_block_sparse_attn(ctypes.byref(p), FAKE, FAKE, FAKE, FAKE, FAKE, -1, FAKE,
-                                        None, None) == 1
+                                        None, None, 0, None) == 1
     assert lib.adaspa_block_sparse_attn(ctypes.byref(p), FAKE, FAKE, FAKE, FAKE,
-                                        ctypes.c_void_p(0x10001), 10, FAKE, None, None) == 1
+                                        ctypes.c_void_p(0x10001), 10, FAKE, None, None, 0, None) == 1
     assert lib.adaspa_block_sparse_attn(ctypes.byref(_prob(head_dim=80)), FAKE, FAKE, FAKE, FAKE,
-                                        FAKE, 10, FAKE, None, None) == 2
+                                        FAKE, 10, FAKE, None, None, 0, None) == 2
+
+
+def test_sparse_workspace_checks(lib):
+    """As for dense attention: the work-queue workspace is optional, and when
+    given it must be large enough and 16-byte aligned."""
+    p = _prob()
+    need = lib.adaspa_block_sparse_attn_workspace(ctypes.byref(p))
+    assert need >= 36 and need % 16 == 0
+    assert lib.adaspa_block_sparse_attn_workspace(ctypes.byref(_prob(head_dim=80))) == 0
+    assert lib.adaspa_block_sparse_attn(ctypes.byref(p), FAKE, FAKE, FAKE, FAKE, FAKE, 10, FAKE,
+                                        None, FAKE, need - 1, None) == 4
+    assert lib.adaspa_block_sparse_attn(ctypes.byref(p), FAKE, FAKE, FAKE, FAKE, FAKE, 10, FAKE,
+                                        None, ctypes.c_void_p(0x10004), need, None) == 4
 
 
 def test_binding_raises_without_library(monkeypatch, tmp_path):

@@ -167,3 +167,26 @@ def test_unordered_rows_take_the_masked_path():
                                                f64(v[0, h]), mask, w.scale)
         check_out(out[0, h, p * 64:(p + 1) * 64], o_ref, f"row {r}")
         check_lse(lse[0, h, p * 64:(p + 1) * 64], l_ref)
+
+
+@pytest.mark.parametrize("block", [64, 128])
+def test_sparse_work_queue_matches_static_split(block):
+    """The queued last tenth of the query blocks only changes which CU runs a
+    block: outputs and LSE are bitwise those of the static split, with a
+    text range and an item count that do not divide by the eight queues,
+    on back-to-back calls that reuse one workspace (each call clears it)."""
+    L = 128 * 61 + 40
+    w = TINY.replace(head_dim=128, heads=3, block=block, seqlen=L, text_len=200,
+                     patches=(L - 200 + 3) // 4)
+    q, k, v = make_qkv(w, device="cuda")
+    nb = w.nblocks
+    tb = text_blocks(L, block, 0, 200)
+    rp, ci = _pattern(w.heads * nb, nb, 9, seed=77, always=tb)
+    rp, ci = rp.cuda(), ci.cuda()
+    txt = dict(text_start=0, text_len=200)
+    o0, l0 = ad.block_sparse_attn(q, k, v, rp, ci, block=block, balance=False, **txt)
+    ws = torch.empty(ad.block_sparse_attn_workspace(q.shape, block), dtype=torch.uint8, device="cuda")
+    for _ in range(3):
+        o1, l1 = ad.block_sparse_attn(q, k, v, rp, ci, block=block, workspace=ws, **txt)
+        torch.cuda.synchronize()
+        assert torch.equal(o0, o1) and torch.equal(l0, l1)
