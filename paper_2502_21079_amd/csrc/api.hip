@@ -90,7 +90,7 @@ WsLayout workspace_layout(const adaspa_problem* p) {
   w.curve = off;  off = align_up(off + bh * nb * sizeof(int64_t));
   w.headk = off;  off = align_up(off + bh * sizeof(int32_t));
   w.base = off;   off = align_up(off + bh * sizeof(int64_t));
-  w.claim = off;  off = align_up(off + 8 * sizeof(uint32_t));   // mass-pass work queues
+  w.claim = off;  off = align_up(off + 9 * sizeof(uint32_t));   // mass-pass work queues (cleared as nine)
   w.total = off;
   return w;
 }
