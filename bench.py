@@ -39,14 +39,13 @@ PEAK_HBM_GBS = 8000.0
 def measured_traffic(kind: str):
     """HBM bytes per launch of a kernel from the committed rocprofv3 record
     (FETCH_SIZE and WRITE_SIZE, scaled by a plain-copy calibration), or None
-    when the kernel sources changed since the counters were taken."""
+    when the library that runs is not the one the counters were taken with
+    (any change to the compiled code changes its hash)."""
     path = os.path.join(ROOT, "profiles", "hbm_traffic.json")
     try:
         rec = json.load(open(path))
-        h = hashlib.sha256()
-        for f in rec["sources"]:
-            h.update(open(os.path.join(ROOT, f), "rb").read())
-        if h.hexdigest()[:16] != rec["source_sha256_16"]:
+        h = hashlib.sha256(open(ad.library_path(), "rb").read()).hexdigest()[:16]
+        if h != rec["library_sha256_16"]:
             return None
         return rec["kernels"][kind]["total_bytes"]
     except (OSError, KeyError, ValueError):

@@ -3,7 +3,7 @@
 //
 // Pipeline.  K/V tiles of 64 keys sit in LDS rings and are filled by direct
 // global->LDS buffer loads (no register staging), issued one or two steps
-// before the tiles are read and spread over the MFMA slots of a step.  Only a
+// before the tiles are read, one per MFMA slot at the front of a step.  Only a
 // tile that reaches past the end of the sequence pays for key masking.
 #include "attn_tile.hpp"
 
@@ -220,8 +220,8 @@ __global__ __launch_bounds__(64 * NW, NW >= 8 ? 1 : 2) void attn_fwd_kernel(Attn
     // Step t reads K(t+1) and V(t-1) from slot (t+1)&1 and loads K(t+2) and
     // V(t) into slot t&1, which step t-1 read: a slot is refilled only after
     // the barrier that follows the step which read it, and a loaded tile is
-    // read only after the barrier that follows its loads.  The loads are
-    // spread over the MFMA slots of the step.  Past the last tile the K
+    // read only after the barrier that follows its loads.  The loads take
+    // the first MFMA slots of the step, one per slot.  Past the last tile the K
     // index is clamped to the last one (an in-range load into a slot that is
     // not read again), so no load depends on a branch.
     auto step = [&](int t, auto sync) {
@@ -828,6 +828,9 @@ __global__ __launch_bounds__(256, 2) void block_mass_kernel(MassParams a) {
       uint32_t fill = lds_addr(ldK);
       asm volatile("" : "+s"(fill));
       auto loads = [&](int slot) {
+        // Load n goes to slot n * NM / NTOT: spread over the whole step here
+        // (front-loaded as in attn_fwd_kernel this exp-heavy pass ran 3-5%
+        // slower).
         constexpr int NTOT = KLoader<D, NW>::PW, NM = 2 * NK;
         static_assert(NTOT <= NM, "one load instruction per slot at most");
         const int n = (slot * NTOT + NM - 1) / NM;

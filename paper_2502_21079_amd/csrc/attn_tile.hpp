@@ -390,11 +390,10 @@ __device__ __forceinline__ void pv_tile(const u16* vlane, const bf16x8 (&pb)[2][
 // the same accumulator are 4 (QK) or 2*ND (PV) slots apart and one wave alone
 // keeps the matrix pipe busy; each accumulator still sums in the same order.
 // Each slot first issues the LDS operand reads of the slot LA places ahead,
-// then its MFMA, then hook(slot) (the caller's tile loads, spread over the
-// step so the load path never stalls the wave for long), then an equal share
-// of the exponentials of the current tile against the reference mc; a
-// scheduling fence closes the slot, so the matrix pipe and the VALU work side
-// by side within the wave.  tsum returns this lane's sum of the tile's
+// then its MFMA, then hook(slot) (the caller's tile loads, at most one per
+// slot), then its share of the softmax of the current tile against the
+// reference mc (below); a scheduling fence closes the slot, so the matrix
+// pipe and the VALU work side by side within the wave.  tsum returns this lane's sum of the tile's
 // rounded probabilities; the caller checks it against the reference's limit.
 template <int D, int KS, int VS, typename Hook>
 __device__ __forceinline__ void pipelined_step(Hook&& hook, const u16* klane, const u16* vlane,
