@@ -6,7 +6,7 @@ import torch
 
 import oracle
 import paper_2502_21079_amd as ad
-from workloads import LONG, TINY, make_qkv, random_block_lists, text_blocks
+from workloads import LONG, MODERATE, TINY, make_qkv, random_block_lists, text_blocks
 from _helpers import check_lse, check_out, f64, sample_blocks
 
 pytestmark = pytest.mark.gpu
@@ -190,3 +190,28 @@ def test_sparse_work_queue_matches_static_split(block):
         o1, l1 = ad.block_sparse_attn(q, k, v, rp, ci, block=block, workspace=ws, **txt)
         torch.cuda.synchronize()
         assert torch.equal(o0, o1) and torch.equal(l0, l1)
+
+
+def test_sparse_moderate_sampled():
+    """The moderate shape (48 heads, L = 17,920, d = 64, block 128) at about
+    20% density with the text sink, sampled query blocks of every sixth head
+    (text blocks and the last block always included)."""
+    w = MODERATE
+    q, k, v = make_qkv(w, device="cuda")
+    nb = w.nblocks
+    tb = text_blocks(w.seqlen, w.block, w.text_start, w.text_len)
+    kk = oracle.topk_count(2000, nb, len(tb))
+    rp, ci = _pattern(w.heads * nb, nb, kk, seed=17, always=tb)
+    out, lse = ad.block_sparse_attn(q, k, v, rp.cuda(), ci.cuda(), block=w.block,
+                                    text_start=w.text_start, text_len=w.text_len)
+    torch.cuda.synchronize()
+    rpn, cin = rp.numpy(), ci.numpy()
+    for h in range(0, w.heads, 6):
+        blocks = sample_blocks(nb, 4, seed=600 + h, always=tuple(tb))
+        o_ref, l_ref = oracle.block_sparse_attention(f64(q[0, h]), f64(k[0, h]), f64(v[0, h]),
+                                                     rpn[h * nb:(h + 1) * nb + 1], cin, w.scale,
+                                                     w.block, qblocks=blocks)
+        rows = np.concatenate([np.arange(p * w.block, min((p + 1) * w.block, w.seqlen)) for p in blocks])
+        idx = torch.as_tensor(rows, device="cuda")
+        check_out(out[0, h, idx], o_ref, f"h{h}")
+        check_lse(lse[0, h, idx], l_ref)
