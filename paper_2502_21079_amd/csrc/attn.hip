@@ -906,6 +906,7 @@ hipError_t launch_dense(AttnParams a, int D, hipStream_t st) {
   a.nqt = (a.seqlen + 255) / 256;
   a.n_items = a.nqt * a.batch_heads;
   a.n_wg = a.n_items;
+  if (a.xcd_map == 2) a.claim = nullptr;     // that mapping takes no items from the queues
   if (a.claim != nullptr) {
     // A quarter more workgroups than items: the XCDs that run ahead take the
     // items the others have not reached; surplus workgroups find every queue
@@ -963,6 +964,7 @@ template <int D, int QB>
 static hipError_t launch_mass_t(MassParams a, hipStream_t st) {
   a.n_items = (a.nkb + QB - 1) / QB * a.batch_heads;
   a.n_wg = a.n_items;
+  if (a.xcd_map == 2) a.claim = nullptr;     // as in launch_dense
   if (a.claim != nullptr) {                  // as in launch_dense
     a.n_wg = a.n_items + (a.n_items + 3) / 4;
     hipLaunchKernelGGL(claim_reset_kernel, dim3(1), dim3(64), 0, st, a.claim);
