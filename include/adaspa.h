@@ -188,6 +188,7 @@ size_t adaspa_block_sparse_attn_workspace(const adaspa_problem* prob);
  * (a repeated block would be counted twice).  prob->text_start/text_len only
  * order the work (the text query blocks, which keep every key block under the
  * text sink, are started first); the results do not depend on them.
+ * Block 64 supports NB <= 8192 key blocks (ADASPA_ERR_UNSUPPORTED otherwise).
  * workspace (optional, caller-owned, 16-byte aligned, at least
  * adaspa_block_sparse_attn_workspace() bytes, contents need not be
  * initialised) holds per-XCD work-queue counters: the last tenth of the query

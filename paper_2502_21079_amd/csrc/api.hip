@@ -306,6 +306,9 @@ adaspa_status adaspa_block_sparse_attn(const adaspa_problem* prob, const void* q
       (lse_out && ((uintptr_t)lse_out & 3u)) || ((uintptr_t)row_ptr & 3u) ||
       ((uintptr_t)col_idx & 3u))
     return ADASPA_ERR_INVALID_ARG;
+  // Block 64 pairs query blocks through a byte map of one row's key blocks
+  // (kMaxBlocks entries); block 128 has no such limit.
+  if (prob->block == 64 && num_blocks(prob) > kMaxBlocks) return ADASPA_ERR_UNSUPPORTED;
   if (workspace && (workspace_bytes < adaspa_block_sparse_attn_workspace(prob) || !aligned16(workspace)))
     return ADASPA_ERR_WORKSPACE;
   AttnParams a;

@@ -174,6 +174,22 @@ def test_sparse_rejects_bad_arguments(lib):
                                         FAKE, 10, FAKE, None, None, 0, None) == 2
 
 
+def test_sparse_block64_block_limit(lib):
+    """Block 64 pairs query blocks through a map of at most 8192 key blocks:
+    longer sequences are refused before anything is enqueued (block 128 is not
+    limited there)."""
+    big64 = _prob(seqlen=8193 * 64, block=64)
+    assert lib.adaspa_block_sparse_attn(ctypes.byref(big64), FAKE, FAKE, FAKE, FAKE, FAKE, 10, FAKE,
+                                        None, None, 0, None) == 2
+    # at the limit the call gets past that check to the (misaligned) workspace
+    edge64 = _prob(seqlen=8192 * 64, block=64)
+    assert lib.adaspa_block_sparse_attn(ctypes.byref(edge64), FAKE, FAKE, FAKE, FAKE, FAKE, 10, FAKE,
+                                        None, ctypes.c_void_p(0x10004), 256, None) == 4
+    big128 = _prob(seqlen=8193 * 128, block=128)
+    assert lib.adaspa_block_sparse_attn(ctypes.byref(big128), FAKE, FAKE, FAKE, FAKE, FAKE, 10, FAKE,
+                                        None, ctypes.c_void_p(0x10004), 256, None) == 4
+
+
 def test_sparse_workspace_checks(lib):
     """As for dense attention: the work-queue workspace is optional, and when
     given it must be large enough and 16-byte aligned."""
