@@ -146,6 +146,7 @@ __global__ __launch_bounds__(64 * NW, NW >= 8 ? 1 : 2) void attn_fwd_kernel(Attn
   };
   int c0 = 0, cid0 = 0, cid1 = 0;
   int skip_at = INT_MAX;      // sparse: pipeline entries at or past it shift by one
+  int rag_sub = 0;            // sparse: full tiles of the ragged entry taken by the pipeline
   if constexpr (SPARSE) {
     const int64_t r = (int64_t)bh * a.nkb + qt;
     int64_t s = a.row_ptr[r], e = a.row_ptr[r + 1];
@@ -166,8 +167,12 @@ __global__ __launch_bounds__(64 * NW, NW >= 8 ? 1 : 2) void attn_fwd_kernel(Attn
       const unsigned long long rb = __ballot(n < ne && ragged && v == a.nkb - 1);
       if (skip < 0 && rb != 0ull) skip = c * 64 + __builtin_ctzll(rb);
     }
-    nf = slow ? 0 : (ne - (skip >= 0 ? 1 : 0)) * SUB;
-    skip_at = skip >= 0 ? skip : INT_MAX;
+    // A ragged block that ends the row (the usual, ascending case) keeps its
+    // full tiles in the pipeline, as the dense kernel does, and only its
+    // partial tile is masked; elsewhere it is left out whole.
+    if (!slow && skip >= 0 && skip == ne - 1) rag_sub = (L - (a.nkb - 1) * a.block) / KT;
+    nf = slow ? 0 : (ne - (skip >= 0 ? 1 : 0)) * SUB + rag_sub;
+    skip_at = (skip >= 0 && skip != ne - 1) ? skip : INT_MAX;
   } else {
     nf = L / KT;
   }
@@ -192,6 +197,12 @@ __global__ __launch_bounds__(64 * NW, NW >= 8 ? 1 : 2) void attn_fwd_kernel(Attn
   f32x16 o[ND];
 #pragma unroll
   for (int d = 0; d < ND; ++d) o[d] = f32x16{};
+  // A wave whose row sums left the safe range redoes its rows on the exact
+  // (masked) path; the workgroup walks the tiles together for the loads and
+  // barriers, and only that wave computes.
+  __shared__ int s_redo;
+  if (tid == 0) s_redo = 0;
+  bool redo = false;                      // this wave redoes its rows
   __syncthreads();
 
   if (nf > 0) {
@@ -212,6 +223,9 @@ __global__ __launch_bounds__(64 * NW, NW >= 8 ? 1 : 2) void attn_fwd_kernel(Attn
       for (int s2 = 0; s2 < 2; ++s2) p_prev[g][s2] = bf16x8{};
     bool pend = false;
     float pend_alpha = 1.f;
+    RowSums rsum;
+    rsum.init(lane);
+    bool bad = false;
 
     LD ld;
     ld.init(wave, lane);
@@ -268,16 +282,9 @@ __global__ __launch_bounds__(64 * NW, NW >= 8 ? 1 : 2) void attn_fwd_kernel(Attn
       };
       f32x16 s_next[2];
       bf16x8 p_cur[2][2];
-      float ts;
       pipelined_step<D, KS, VS>(loads, rdK + klane, rdV + voff, qf, s_cur, p_prev, s_next, p_cur, o, sl2,
-                                ref.mc, ts);
-      if (__any(ts > ref.lim)) {          // rare: the reference moves for this tile
-        pend_alpha = ref.raise(s_cur, sl2);
-        pend = true;
-        lsum *= pend_alpha;
-        ts = exp_tile(s_cur, sl2, ref.mc, p_cur);
-      }
-      lsum += ts;
+                                ref.mc, rsum);
+      move_reference(ref, rsum, bad, s_cur, p_cur, pend, pend_alpha, sl2, c32);
 #pragma unroll
       for (int g = 0; g < 2; ++g) {
         s_cur[g] = s_next[g];
@@ -302,39 +309,59 @@ __global__ __launch_bounds__(64 * NW, NW >= 8 ? 1 : 2) void attn_fwd_kernel(Attn
         for (int e = 0; e < 16; ++e) o[d][e] *= pend_alpha;
     }
     pv_tile<ND, VS>(sV[(nf - 1) & (RING - 1)] + voff, p_prev, o);
+    lsum = finish_sums(rsum, bad, p_prev, hw, c32);
+    redo = __any(bad);
+    if (redo && lane == 0) s_redo = 1;
     __syncthreads();
   }
+  const bool any_redo = s_redo != 0;
+  if (redo) {
+    ref = RowRef{};
+    lsum = 0.f;
+#pragma unroll
+    for (int d = 0; d < ND; ++d) o[d] = f32x16{};
+  }
 
-  // Remaining tiles, one at a time with key masking.
-  auto masked_tile = [&](int kb) {
+  // Remaining tiles, one at a time with key masking (the waves that do not
+  // compute a tile still issue their share of its loads and meet at the
+  // barriers).
+  auto masked_tile = [&](int kb, bool compute) {
     KDMA::issue(rK, sK[0], kb, wave, lane);
     VDMA::issue(rV, sV[0], kb, wave, lane);
     wait_vmem();
     __syncthreads();
-    f32x16 s[2];
-    qk_tile<D, KS>(sK[0], qf, c32, hw, s);
-    mask_tile(s, L - kb, hw);
-    bf16x8 pb[2][2];
-    const float alpha = softmax_tile(s, ref, lsum, sl2, pb);
+    if (compute) {
+      f32x16 s[2];
+      qk_tile<D, KS>(sK[0], qf, c32, hw, s);
+      mask_tile(s, L - kb, hw);
+      bf16x8 pb[2][2];
+      const float alpha = softmax_tile(s, ref, lsum, sl2, pb);
 #pragma unroll
-    for (int d = 0; d < ND; ++d)
+      for (int d = 0; d < ND; ++d)
 #pragma unroll
-      for (int e = 0; e < 16; ++e) o[d][e] *= alpha;
-    pv_tile<ND, VS>(sV[0] + voff, pb, o);
+        for (int e = 0; e < 16; ++e) o[d][e] *= alpha;
+      pv_tile<ND, VS>(sV[0] + voff, pb, o);
+    }
     __syncthreads();
   };
   if constexpr (SPARSE) {
+    // Malformed rows: every entry; otherwise the tiles of the ragged block
+    // the pipeline left out, and every tile for the waves that redo their
+    // rows (in row order either way).
     for (int i = 0; i < ne; ++i) {
-      if (!slow && i != skip) continue;
+      if (!slow && i != skip && !any_redo) continue;
       const int c = a.col_idx[e0 + i];
       if (c < 0 || c >= a.nkb) continue;
       for (int j = 0; j < sub; ++j) {
         const int kb = c * a.block + j * KT;
-        if (kb < L) masked_tile(kb);
+        const bool left = slow || (i == skip && j >= rag_sub);
+        if (kb < L && (left || any_redo)) masked_tile(kb, left || redo);
       }
     }
   } else {
-    if (nf * KT < L) masked_tile(nf * KT);
+    if (any_redo)
+      for (int t = 0; t < nf; ++t) masked_tile(t * KT, redo);
+    if (nf * KT < L) masked_tile(nf * KT, true);
   }
 
   // Normalise and store.
@@ -545,6 +572,9 @@ __global__ __launch_bounds__(64 * NW, NW >= 8 ? 1 : 2) void attn_sparse_pair_ker
 #pragma unroll
       for (int e = 0; e < 16; ++e) s[g][e] = -INFINITY;
   };
+  __shared__ int s_redo;              // as in attn_fwd_kernel
+  if (tid == 0) s_redo = 0;
+  bool redo = false;
   __syncthreads();                    // block map reads done
 
   if (nf > 0) {
@@ -573,6 +603,9 @@ __global__ __launch_bounds__(64 * NW, NW >= 8 ? 1 : 2) void attn_sparse_pair_ker
       for (int s2 = 0; s2 < 2; ++s2) p_prev[g][s2] = bf16x8{};
     bool pend = false;
     float pend_alpha = 1.f;
+    RowSums rsum;
+    rsum.init(lane);
+    bool bad = false;
     LD ld;
     ld.init(wave, lane);
     const u32x4 rMw = ld.mixed_v ? rVw : rKw;     // resource of this wave's mixed entry
@@ -608,16 +641,9 @@ __global__ __launch_bounds__(64 * NW, NW >= 8 ? 1 : 2) void attn_sparse_pair_ker
       };
       f32x16 s_next[2];
       bf16x8 p_cur[2][2];
-      float ts;
       pipelined_step<D, KS, VS>(loads, rdK + klane, rdV + voff, qf, s_cur, p_prev, s_next, p_cur, o, sl2,
-                                ref.mc, ts);
-      if (__any(ts > ref.lim)) {          // rare: the reference moves for this tile
-        pend_alpha = ref.raise(s_cur, sl2);
-        pend = true;
-        lsum *= pend_alpha;
-        ts = exp_tile(s_cur, sl2, ref.mc, p_cur);
-      }
-      lsum += ts;
+                                ref.mc, rsum);
+      move_reference(ref, rsum, bad, s_cur, p_cur, pend, pend_alpha, sl2, c32);
 #pragma unroll
       for (int g = 0; g < 2; ++g) {
         s_cur[g] = s_next[g];
@@ -649,41 +675,56 @@ __global__ __launch_bounds__(64 * NW, NW >= 8 ? 1 : 2) void attn_sparse_pair_ker
         for (int e = 0; e < 16; ++e) o[d][e] *= pend_alpha;
     }
     pv_tile<ND, VS>(sV[(nf - 1) & 1] + voff, p_prev, o);
+    lsum = finish_sums(rsum, bad, p_prev, hw, c32);
+    redo = __any(bad);
+    if (redo && lane == 0) s_redo = 1;
     __syncthreads();
   }
+  const bool any_redo = s_redo != 0;
+  if (redo) {
+    ref = RowRef{};
+    lsum = 0.f;
+#pragma unroll
+    for (int d = 0; d < ND; ++d) o[d] = f32x16{};
+  }
 
-  // One tile with key masking, kept by the rows in keep.
-  auto masked_tile = [&](int kb, int keep) {
+  // One tile with key masking, kept by the rows in keep (computed by the
+  // waves in compute; the others only load and meet at the barriers).
+  auto masked_tile = [&](int kb, int keep, bool compute) {
     KDMA::issue(rK, sK[0], kb, wave, lane);
     VDMA::issue(rV, sV[0], kb, wave, lane);
     wait_vmem();
     __syncthreads();
-    f32x16 s[2];
-    qk_tile<D, KS>(sK[0], qf, c32, hw, s);
-    mask_tile(s, L - kb, hw);
-    if (!(keep & mybit)) hide(s);
-    bf16x8 pb[2][2];
-    const float alpha = softmax_tile(s, ref, lsum, sl2, pb);
+    if (compute) {
+      f32x16 s[2];
+      qk_tile<D, KS>(sK[0], qf, c32, hw, s);
+      mask_tile(s, L - kb, hw);
+      if (!(keep & mybit)) hide(s);
+      bf16x8 pb[2][2];
+      const float alpha = softmax_tile(s, ref, lsum, sl2, pb);
 #pragma unroll
-    for (int d = 0; d < ND; ++d)
+      for (int d = 0; d < ND; ++d)
 #pragma unroll
-      for (int e = 0; e < 16; ++e) o[d][e] *= alpha;
-    pv_tile<ND, VS>(sV[0] + voff, pb, o);
+        for (int e = 0; e < 16; ++e) o[d][e] *= alpha;
+      pv_tile<ND, VS>(sV[0] + voff, pb, o);
+    }
     __syncthreads();
   };
-  if (slow) {
-    // Malformed rows: each row's valid entries in its own order.
+  if (slow || any_redo) {
+    // Malformed rows, or waves that redo their rows: each row's valid
+    // entries in its own order.
 #pragma unroll
     for (int r = 0; r < 2; ++r)
       for (int i = 0; i < len[r]; ++i) {
         const int c = a.col_idx[beg[r] + i];
         if (c >= 0 && c < nkb)
           for (int j = 0; j < SUB; ++j)
-            if (c * BLK + j * KT < L) masked_tile(c * BLK + j * KT, 1 << r);
+            if (c * BLK + j * KT < L) masked_tile(c * BLK + j * KT, 1 << r, slow || redo);
       }
-  } else if (rag) {
+  }
+  if (!slow && rag) {
     for (int j = 0; j < SUB; ++j)
-      if ((nkb - 1) * BLK + j * KT < L) masked_tile((nkb - 1) * BLK + j * KT, rag);
+      if ((nkb - 1) * BLK + j * KT < L) masked_tile((nkb - 1) * BLK + j * KT, rag, !redo);
   }
 
   float lt;

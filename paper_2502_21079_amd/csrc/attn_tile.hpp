@@ -12,10 +12,10 @@
 // V^T operand is read from a row-major V tile with the LDS transpose read.
 //
 // Online softmax.  Probabilities are taken against a per-row reference that
-// moves only when a tile's probabilities grow too large (checked per 32 rows
-// from their sum), so neither a per-tile maximum nor a rescale of the output
-// accumulator is needed for almost every tile; the final normalisation uses
-// the same reference, so the result is unchanged.
+// moves only when a row's running sum grows too large, so neither a per-tile
+// maximum nor a rescale of the output accumulator is needed for almost every
+// tile; the final normalisation uses the same reference, so the result is
+// unchanged.  The running sums are formed on the matrix pipe (RowSums).
 #pragma once
 
 #include <type_traits>
@@ -30,6 +30,7 @@ constexpr int KT = 64;          // keys per tile
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
 typedef __attribute__((address_space(3))) void lds_void;
+typedef float f32x4 __attribute__((ext_vector_type(4)));
 
 __device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void* base, uint32_t bytes) {
   return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), 0, bytes, 0x00020000);
@@ -239,6 +240,7 @@ __device__ __forceinline__ float vmax(float a, float b) { return __builtin_eleme
 // compiler can neither sink the work that produces v past them (out of the
 // MFMA slot it was placed in) nor hoist it.
 __device__ __forceinline__ void pin(float& v) { asm volatile("" : "+v"(v)); }
+__device__ __forceinline__ void pin(bf16x2& v) { asm volatile("" : "+v"(v)); }
 
 __device__ __forceinline__ void wait_vmem() { __builtin_amdgcn_s_waitcnt(0x0F70); }   // vmcnt(0)
 
@@ -287,16 +289,17 @@ __device__ __forceinline__ void zero_lds(u16* p, int tid, int nt) {
 
 // Online softmax against a lazy reference.  Probabilities of a row are taken
 // as exp2(s * sl2 - mc) with mc = m * sl2 for a reference m (raw score units)
-// that is NOT the running maximum: it moves only when the probabilities of a
-// tile, summed over one lane's keys, exceed kTileSumLimit, and on every tile
-// while m is still -inf (the first tile with a finite score sets it to that
-// tile's maximum, however negative: against mc = 0 a row whose scaled scores
-// all lie below the fp32 exponent range would otherwise sum to zero and never
-// set it), so no per-tile maximum is computed on the common path.  Every
-// probability then stays below 2^16 (no overflow of the fp32 sums), and the
-// final normalisation uses the same reference, so the result is the softmax
-// whatever the reference.  When the reference moves, sums taken against the
-// old one are rescaled by exp2((m_old - m_new) * sl2).
+// that is NOT the running maximum, so no per-tile maximum is computed on the
+// common path; the final normalisation uses the same reference, so the
+// result is the softmax whatever the reference.  The first tile with a finite
+// score sets it to that tile's maximum, however negative (against mc = 0 a
+// row whose scaled scores all lie below the fp32 exponent range would sum to
+// zero).  In the pipeline it then moves only when the row's running sum
+// passes kRowSumLimit (move_reference below); on the masked, exact path it
+// moves when the tile's probabilities, summed over one lane's keys, exceed
+// kTileSumLimit (RowRef::lim, checked before the tile enters P V), so there no
+// probability exceeds 2^16 whatever the scores.  When the reference moves,
+// sums taken against the old one are rescaled.
 constexpr float kTileSumLimit = 65536.f;
 
 struct RowRef {
@@ -323,6 +326,45 @@ struct RowRef {
     lim = (m == -INFINITY) ? -1.f : kTileSumLimit;
     return a;
   }
+  // Moves a set reference up by d (log2 units): sums taken against the old
+  // one scale by 2^-d.
+  __device__ __forceinline__ void shift(float d, float sl2) {
+    mc += d;
+    m = mc / sl2;
+  }
+};
+
+// Running row sums of the rounded probabilities, formed on the matrix pipe.
+// The 16x16x32 bf16 MFMA takes a P^T operand of the P V product as its B
+// operand (lane l holds 8 keys of query row l % 32, so output column n
+// gathers lanes n, n+16, n+32 and n+48, i.e. rows n and n+16) and a 0/1
+// selector as A: output rows 0-7 keep k-groups 0 and 2 (lanes n, n+32:
+// row n), output rows 8-15 keep k-groups 1 and 3 (row n+16).  Lane l then
+// holds the sum of query row (l % 16) + 16 (l / 32), the same in all four
+// accumulator entries.  (A v_dot2c per pair on the VALU holds the matrix
+// pipe ~20 cycles each; four of these MFMAs take 64 cycles per step.)
+// Sums above kRowSumLimit move the reference by log2 of the sum; a sum above
+// kRowSumBad (or not finite) means a single tile jumped so far above the
+// reference that a product may have overflowed, and the caller redoes the
+// row on the exact path.
+constexpr float kRowSumLimit = 1099511627776.f;                   // 2^40
+constexpr float kRowSumBad = 1267650600228229401496703205376.f;   // 2^100
+
+struct RowSums {
+  f32x4 acc;
+  bf16x8 sel;
+  __device__ __forceinline__ void init(int lane) {
+    acc = f32x4{0.f, 0.f, 0.f, 0.f};
+    const __bf16 v = (((lane & 15) < 8) == (((lane >> 4) & 1) == 0)) ? (__bf16)1.0f : (__bf16)0.0f;
+    sel = bf16x8{v, v, v, v, v, v, v, v};
+  }
+  __device__ __forceinline__ void add(const bf16x8& p) {
+    acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(sel, p, acc, 0, 0, 0);
+  }
+  // The sum of query row c32 (the row of the P V layout), from its lane.
+  __device__ __forceinline__ static float for_row(float v, int c32) {
+    return __shfl(v, c32 < 16 ? c32 : c32 + 16, 64);
+  }
 };
 
 // P = bf16(exp2(s * sl2 - mc)) for one S^T tile; returns this lane's sum of
@@ -342,6 +384,50 @@ __device__ __forceinline__ float exp_tile(const f32x16 (&s)[2], float sl2, float
       ts = __builtin_amdgcn_fdot2_f32_bf16(pr, ones, ts, false);
     }
   return ts;
+}
+
+// End of a pipelined step (rare branch, taken by the whole wave): rows whose
+// running sum (tiles up to the previous one) passed kRowSumLimit move their
+// reference up by log2 of the sum, so the sum becomes about 1; rows without a
+// reference yet take this tile's maximum (their sums so far are 0).  The sums
+// are rescaled here, the output accumulator at the start of the next step
+// (pend), and the current tile's probabilities are taken again against the
+// new reference.  bad is set when a sum has left the safe range.
+__device__ __forceinline__ void move_reference(RowRef& ref, RowSums& rsum, bool& bad,
+                                               const f32x16 (&s_cur)[2], bf16x8 (&p_cur)[2][2],
+                                               bool& pend, float& pend_alpha, float sl2, int c32) {
+  const float sr = rsum.acc[0];
+  if (!__any(ref.m == -INFINITY || sr > kRowSumLimit)) return;
+  bad = bad || !(sr <= kRowSumBad);
+  const float dr = sr > kRowSumLimit ? __builtin_amdgcn_logf(sr) : 0.f;   // log2 of the sum
+  const float ar = fast_exp2(-dr);
+#pragma unroll
+  for (int j = 0; j < 4; ++j) rsum.acc[j] *= ar;
+  const float d = RowSums::for_row(dr, c32);        // the same value for this lane's row
+  float al;
+  if (ref.m == -INFINITY) {
+    al = ref.raise(s_cur, sl2);
+  } else {
+    if (d > 0.f) ref.shift(d, sl2);
+    al = fast_exp2(-d);
+  }
+  pend_alpha = al;
+  pend = true;
+  exp_tile(s_cur, sl2, ref.mc, p_cur);
+}
+
+// After the last pipelined tile: its probabilities join the sums, a sum out
+// of the safe range sets bad, and the row's sum is returned in the form the
+// masked path continues from (the whole sum on the hw = 0 lane of the row, 0
+// on the other).
+__device__ __forceinline__ float finish_sums(RowSums& rsum, bool& bad, const bf16x8 (&p_last)[2][2],
+                                             int hw, int c32) {
+#pragma unroll
+  for (int j = 0; j < 4; ++j) rsum.add(p_last[j >> 1][j & 1]);
+  const float sr = rsum.acc[0];
+  bad = bad || !(sr <= kRowSumBad);
+  const float v = RowSums::for_row(sr, c32);
+  return hw == 0 ? v : 0.f;
 }
 
 // Softmax of one tile outside the pipeline (masked tiles): P against the
@@ -393,14 +479,15 @@ __device__ __forceinline__ void pv_tile(const u16* vlane, const bf16x8 (&pb)[2][
 // then its MFMA, then hook(slot) (the caller's tile loads, at most one per
 // slot), then its share of the softmax of the current tile against the
 // reference mc (below); a scheduling fence closes the slot, so the matrix
-// pipe and the VALU work side by side within the wave.  tsum returns this lane's sum of the tile's
-// rounded probabilities; the caller checks it against the reference's limit.
+// pipe and the VALU work side by side within the wave.  Four slots also add
+// the previous tile's rounded probabilities (the operands of its P V) to the
+// running row sums.
 template <int D, int KS, int VS, typename Hook>
 __device__ __forceinline__ void pipelined_step(Hook&& hook, const u16* klane, const u16* vlane,
                                                const bf16x8 (&qf)[D / 16], const f32x16 (&s_cur)[2],
                                                const bf16x8 (&p_prev)[2][2], f32x16 (&s_next)[2],
                                                bf16x8 (&p_cur)[2][2], f32x16 (&o)[D / 32], float sl2,
-                                               float mc, float& tsum) {
+                                               float mc, RowSums& rsum) {
   constexpr int NK = D / 16, ND = D / 32;
   constexpr int NQK = 2 * NK, NPV = 4 * ND;
   static_assert(NQK == NPV, "QK and PV slots alternate");
@@ -438,12 +525,11 @@ __device__ __forceinline__ void pipelined_step(Hook&& hook, const u16* klane, co
   // Slot i owns scores e in [i*PER, (i+1)*PER) of the tile's 32, in (group,
   // element) order.  Their softmax is pipelined over three slots: slot i
   // forms the exponent arguments, slot i+1 takes the exponentials, slot i+2
-  // rounds each completed pair to bf16 and adds it to the row sum, so no
-  // instruction waits on the result of the one just before it.  The last
-  // two slots' shares are finished after the MFMAs.
+  // rounds each completed pair to bf16, so no instruction waits on the result
+  // of the one just before it.  The last two slots' shares are finished after
+  // the MFMAs.
   constexpr int PER = 32 / NM;
-  const bf16x2 ones = {(__bf16)1.0f, (__bf16)1.0f};
-  float ts = 0.f;
+  constexpr int RSP = NM / 4;                 // row-sum MFMAs in slots RSP/2 + j*RSP
   float arg[32], ex[32];
   auto stage_arg = [&](int i) {
 #pragma unroll
@@ -466,11 +552,10 @@ __device__ __forceinline__ void pipelined_step(Hook&& hook, const u16* klane, co
     for (int u = 0; u < PER; ++u) {
       const int e = i * PER + u, g = e >> 4, r = e & 15;
       if (e & 1) {
-        const bf16x2 pr = {(__bf16)ex[e - 1], (__bf16)ex[e]};
+        bf16x2 pr = {(__bf16)ex[e - 1], (__bf16)ex[e]};
+        pin(pr);
         p_cur[g][r >> 3][(r & 7) - 1] = pr[0];
         p_cur[g][r >> 3][r & 7] = pr[1];
-        ts = __builtin_amdgcn_fdot2_f32_bf16(pr, ones, ts, false);
-        pin(ts);
       }
     }
   };
@@ -481,6 +566,7 @@ __device__ __forceinline__ void pipelined_step(Hook&& hook, const u16* klane, co
   for (int i = 0; i < NM; ++i) {
     if (i + LA < NM) fetch(i + LA);
     mfma(i);
+    if (i % RSP == RSP / 2) rsum.add(p_prev[(i / RSP) >> 1][(i / RSP) & 1]);
     hook(i);
     stage_arg(i);
     if (i >= 1) stage_exp(i - 1);
@@ -490,7 +576,6 @@ __device__ __forceinline__ void pipelined_step(Hook&& hook, const u16* klane, co
   stage_exp(NM - 1);
   stage_sum(NM - 2);
   stage_sum(NM - 1);
-  tsum = ts;
 }
 
 // One pipelined step of the block-mass pass: the NM = 2*NK QK MFMAs of the
