@@ -127,6 +127,16 @@ __global__ __launch_bounds__(64 * NW, NW >= 8 ? 1 : 2) void attn_fwd_kernel(Attn
   bf16x8 qf[NK];
   load_q<D>(a.q + hoff, qrow, L, hw, qf);
 
+  // Sparse rows ordered with a text range start, under the text sink, with
+  // the first text block: its first two tiles are loaded into place before
+  // the row's indices are read (a guess, checked below), which takes the
+  // index round trips off the path to the first tile.
+  const int spec = (SPARSE && a.tq1 > a.tq0) ? a.tq0 * a.block : -1;
+  if (spec >= 0) {
+    KDMA::issue(rK, sK[0], spec, wave, lane);
+    KDMA::issue(rK, sK[1], spec + KT, wave, lane);
+  }
+
   // Tiles: nf full tiles through the pipeline; the rest one by one, masked.
   int nf = 0;                 // full tiles in the pipeline
   int e0 = 0, ne = 0;         // sparse: CSR entries [e0, e0 + ne)
@@ -207,9 +217,14 @@ __global__ __launch_bounds__(64 * NW, NW >= 8 ? 1 : 2) void attn_fwd_kernel(Attn
 
   if (nf > 0) {
     // Step t reads K(t+1) and V(t-1), so the first steps need K(0) and K(1)
-    // in place.
-    KDMA::issue(rK, sK[0], kbase(0), wave, lane);
-    if (nf > 1) KDMA::issue(rK, sK[1], kbase(1), wave, lane);
+    // in place.  A wrong guess is overwritten once this wave's guessed loads
+    // have landed (each wave reloads the same pieces of the slots).
+    const int kb0 = kbase(0), kb1 = nf > 1 ? kbase(1) : -1;
+    if (!(spec >= 0 && kb0 == spec && (nf < 2 || kb1 == spec + KT))) {
+      if (spec >= 0) wait_vmem();
+      KDMA::issue(rK, sK[0], kb0, wave, lane);
+      if (nf > 1) KDMA::issue(rK, sK[1], kb1, wave, lane);
+    }
     wait_vmem();
     __syncthreads();
     f32x16 s_cur[2];
@@ -348,16 +363,21 @@ __global__ __launch_bounds__(64 * NW, NW >= 8 ? 1 : 2) void attn_fwd_kernel(Attn
     // Malformed rows: every entry; otherwise the tiles of the ragged block
     // the pipeline left out, and every tile for the waves that redo their
     // rows (in row order either way).
-    for (int i = 0; i < ne; ++i) {
-      if (!slow && i != skip && !any_redo) continue;
+    auto entry_tiles = [&](int i) {
       const int c = a.col_idx[e0 + i];
-      if (c < 0 || c >= a.nkb) continue;
+      if (c < 0 || c >= a.nkb) return;
       for (int j = 0; j < sub; ++j) {
         const int kb = c * a.block + j * KT;
         const bool left = slow || (i == skip && j >= rag_sub);
         if (kb < L && (left || any_redo)) masked_tile(kb, left || redo);
       }
+    };
+    if (slow || any_redo) {
+      for (int i = 0; i < ne; ++i) entry_tiles(i);
+    } else if (skip >= 0) {
+      entry_tiles(skip);
     }
+    if (nf == 0 && spec >= 0) wait_vmem();    // no guessed load is left in flight
   } else {
     if (any_redo)
       for (int t = 0; t < nf; ++t) masked_tile(t * KT, redo);
