@@ -337,6 +337,8 @@ adaspa_status adaspa_block_sparse_attn(const adaspa_problem* prob, const void* q
     a.tq1 = (prob->text_start + prob->text_len + prob->block - 1) / prob->block;
     if (a.tq1 - a.tq0 >= a.nkb) a.tq0 = a.tq1 = 0;    // every row is text: plain order
   }
+  a.kb_guess = a.tq1 > a.tq0 ? a.tq0 : -1;
+  a.n_guess = a.tq1 - a.tq0;
   return launch_sparse(a, prob->head_dim, (hipStream_t)stream) == hipSuccess ? ADASPA_OK : ADASPA_ERR_HIP;
 }
 

@@ -131,7 +131,7 @@ __global__ __launch_bounds__(64 * NW, NW >= 8 ? 1 : 2) void attn_fwd_kernel(Attn
   // the first text block: its first two tiles are loaded into place before
   // the row's indices are read (a guess, checked below), which takes the
   // index round trips off the path to the first tile.
-  const int spec = (SPARSE && a.tq1 > a.tq0) ? a.tq0 * a.block : -1;
+  const int spec = (SPARSE && a.kb_guess >= 0) ? a.kb_guess * a.block : -1;
   if (spec >= 0) {
     KDMA::issue(rK, sK[0], spec, wave, lane);
     KDMA::issue(rK, sK[1], spec + KT, wave, lane);
@@ -474,6 +474,13 @@ __global__ __launch_bounds__(64 * NW, NW >= 8 ? 1 : 2) void attn_sparse_pair_ker
   for (int b = 0; b < 2; ++b) zero_lds<VDMA::SLOTS>(sV[b], tid, NT);   // finite V; the block map
   bf16x8 qf[NK];
   load_q<D>(a.q + hoff, qrow, L, hw, qf);
+  // As in attn_fwd_kernel: under the text sink the union of the two rows
+  // begins with the text blocks, so its first two tiles are loaded on a guess
+  // before the indices are read (checked before the first tile is used).
+  const int g0 = a.kb_guess >= 0 ? a.kb_guess * BLK : -1;
+  const int g1 = g0 < 0 ? -1 : (SUB > 1 ? g0 + KT : (a.n_guess >= 2 ? g0 + BLK : -1));
+  if (g0 >= 0) KDMA::issue(rK, sK[0], g0, wave, lane);
+  if (g1 >= 0) KDMA::issue(rK, sK[1], g1, wave, lane);
 
   // The two rows.  Each row's indices are read 64 at a time into one
   // register per lane through a resource bounded to the row (lanes past its
@@ -607,8 +614,12 @@ __global__ __launch_bounds__(64 * NW, NW >= 8 ? 1 : 2) void attn_sparse_pair_ker
     auto pick = [&](const int (&x)[3], int slot) { return slot == 0 ? x[0] : (slot == 1 ? x[1] : x[2]); };
     // First row of pipeline tile j, j within the queue's reach.
     auto tile_row = [&](int j) { return (pick(ub, j / SUB - u0) * SUB + j % SUB) * KT; };
-    KDMA::issue(rK, sK[0], tile_row(0), wave, lane);
-    if (nf > 1) KDMA::issue(rK, sK[1], tile_row(1), wave, lane);
+    const int r0 = tile_row(0), r1 = nf > 1 ? tile_row(1) : -1;
+    if (!(g0 >= 0 && r0 == g0 && (nf < 2 || r1 == g1))) {
+      if (g0 >= 0) wait_vmem();          // this wave's guessed loads land first
+      KDMA::issue(rK, sK[0], r0, wave, lane);
+      if (nf > 1) KDMA::issue(rK, sK[1], r1, wave, lane);
+    }
     wait_vmem();
     __syncthreads();
     f32x16 s_cur[2];
@@ -746,6 +757,7 @@ __global__ __launch_bounds__(64 * NW, NW >= 8 ? 1 : 2) void attn_sparse_pair_ker
     for (int j = 0; j < SUB; ++j)
       if ((nkb - 1) * BLK + j * KT < L) masked_tile((nkb - 1) * BLK + j * KT, rag, !redo);
   }
+  if (nf == 0 && g0 >= 0) wait_vmem();      // no guessed load is left in flight
 
   float lt;
   {

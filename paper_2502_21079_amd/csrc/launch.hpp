@@ -28,6 +28,8 @@ struct AttnParams {
   int xcd_map;                // 0 hardware order, 1 contiguous per XCD, 2 head-chunked,
                               // 3 sparse: text first, then head-chunked
   int tq0, tq1;               // sparse: text query blocks [tq0, tq1), dispatched first
+  int kb_guess, n_guess;      // sparse: first text block and the text block count (-1, 0: none),
+                              // whose tiles every row begins with under the text sink
   uint32_t* claim;            // 9 work-queue counters (one per XCD + a flag), or null
   int n_items;                // work items: (head, query tile) or (head, query block / pair)
   int n_static;               // sparse: items [0, n_static) run in the static order
