@@ -29,7 +29,8 @@ def test_dense_extreme_scores(kind, D, L):
 
 
 @pytest.mark.parametrize("kind", EXTREME_KINDS)
-@pytest.mark.parametrize("D,block,L,kb", [(64, 64, 1000, 5), (128, 128, 777, 3), (128, 64, 777, 4)])
+@pytest.mark.parametrize("D,block,L,kb", [(64, 64, 1000, 5), (128, 128, 777, 3), (128, 64, 777, 4),
+                                           (64, 128, 1000, 8)])
 def test_sparse_extreme_scores(kind, D, block, L, kb):
     (q, k, v), scale = make_extreme_qkv(kind, heads=2, seqlen=L, head_dim=D, device="cuda")
     nb = (L + block - 1) // block
@@ -47,9 +48,13 @@ def test_sparse_extreme_scores(kind, D, block, L, kb):
 
 @pytest.mark.parametrize("kind", EXTREME_KINDS)
 @pytest.mark.parametrize("block", [64, 128])
-def test_all_blocks_equals_dense_extreme(kind, block):
-    (q, k, v), scale = make_extreme_qkv(kind, heads=2, seqlen=900, head_dim=64, device="cuda")
-    nb = (900 + block - 1) // block
+@pytest.mark.parametrize("L", [900, 1000])
+def test_all_blocks_equals_dense_extreme(kind, block, L):
+    """Keeping every block equals dense bit for bit, also where waves redo
+    their rows on the exact path; at L = 1000 the last block of 128 holds a
+    full tile that both kernels take through the pipeline."""
+    (q, k, v), scale = make_extreme_qkv(kind, heads=2, seqlen=L, head_dim=64, device="cuda")
+    nb = (L + block - 1) // block
     od, ld = ad.dense_attn_lse(q, k, v, scale=scale)
     rp = (torch.arange(2 * nb + 1, dtype=torch.int32) * nb).cuda()
     ci = torch.arange(nb, dtype=torch.int32).repeat(2 * nb).cuda()
