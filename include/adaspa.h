@@ -187,7 +187,10 @@ size_t adaspa_block_sparse_attn_workspace(const adaspa_problem* prob);
  * patterns never read out of bounds.  Rows should be strictly ascending
  * (a repeated block would be counted twice).  prob->text_start/text_len only
  * order the work (the text query blocks, which keep every key block under the
- * text sink, are started first); the results do not depend on them.
+ * text sink, are started first) and name the block every row is expected to
+ * begin with (its first tiles are loaded before the row's indices are read,
+ * and reloaded if the row begins elsewhere); the results do not depend on
+ * them.
  * Block 64 supports NB <= 8192 key blocks (ADASPA_ERR_UNSUPPORTED otherwise).
  * workspace (optional, caller-owned, 16-byte aligned, at least
  * adaspa_block_sparse_attn_workspace() bytes, contents need not be
