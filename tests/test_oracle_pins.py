@@ -256,9 +256,14 @@ def test_selection_matches_brute_force_sort(seed, ties, text):
     nb = 8
     W = random_block_masses((1, 3, nb, nb), seed, ties=ties).numpy()
     tset = oracle.text_block_set(512, 64, *text)
-    for keep in (0, 1, 1250, 3000, 5000, 9999, 10000):
+    # Counts worked out by hand for NB = 8: ceil(keep * 8 / 10000) is 0, 1, 1,
+    # 3, 4, 8, 8 for these keep fractions, raised to at least one block and to
+    # at least the forced text blocks (two for the unaligned range 100..139).
+    kmin = 2 if text == (100, 40) else 1
+    expect_k = dict(zip((0, 1, 1250, 3000, 5000, 9999, 10000),
+                        [max(kmin, x) for x in (0, 1, 1, 3, 4, 8, 8)]))
+    for keep, k in expect_k.items():
         sel = oracle.select_blocks(W, 512, 64, text[0], text[1], "topk", [keep] * 3)
-        k = max(max(1, len(tset)), min(nb, -(-keep * nb // 10000)))
         for h in range(3):
             assert sel["head_k"][0, h] == k
             got = [sel["col_idx"][sel["row_ptr"][h * nb + p]:sel["row_ptr"][h * nb + p + 1]].tolist()
@@ -366,3 +371,103 @@ def test_hierarchical_mode_levels():
         expect[h] = 6          # sparsity 0.7 -> keep 30% of 20
     assert sel["head_k"][0].tolist() == expect
     assert n >= 1
+
+
+# --- hand-derived values for the remaining oracle functions ----------------
+
+def test_recall_worked_example(worked):
+    """Recall equation (Sec. 2.3): kept mass over total mass, from the block
+    masses of the worked example.  Without text sink the top-1 rows keep
+    W[0,1] and W[1,0]: (5/4 + 5/4) / 4 = 5/8; with the text sink block row 0
+    is a text row kept whole: (2 + 5/4) / 4 = 13/16.  Keeping everything gives
+    1 and keeping nothing 0."""
+    g, q, k, v = worked
+    _, lse = oracle.dense_attention(q, k, v, 1.0)
+    W = oracle.block_mass(q, k, lse, 1.0, 2)
+    assert oracle.recall(W, [[1], [0]]) == pytest.approx(_frac(g["no_text"]["recall"]), abs=1e-15)
+    assert oracle.recall(W, [[0, 1], [0]]) == pytest.approx(_frac(g["text_sink"]["recall"]), abs=1e-15)
+    assert oracle.recall(W, [[0, 1], [0, 1]]) == pytest.approx(1.0, abs=1e-15)
+    assert oracle.recall(W, [[], []]) == 0.0
+    # a row listed out of order counts the same blocks
+    assert oracle.recall(W, [[1, 0], [0]]) == pytest.approx(13 / 16, abs=1e-15)
+
+
+@pytest.mark.parametrize("rng_,block,expect", [
+    ((100, 40), 64, {1, 2}),        # tokens 100..139: blocks [64,128) and [128,192)
+    ((63, 2), 64, {0, 1}),          # tokens 63, 64 straddle the first boundary
+    ((64, 64), 64, {1}),            # exactly block 1
+    ((127, 1), 64, {1}),            # the last token of block 1
+    ((128, 1), 64, {2}),            # the first token of block 2
+    ((0, 1), 64, {0}),
+    ((0, 256), 128, {0, 1}),        # the long-video text range at block 128
+    ((0, 256), 64, {0, 1, 2, 3}),   # ... and at block 64
+    ((1000, 300), 128, {7, 8, 9, 10}),   # tokens 1000..1299: blocks 7 (896..1023) to 10 (1280..1407)
+    ((500, 0), 64, set()),          # no text
+])
+def test_text_block_set_hand_derived(rng_, block, expect):
+    """Text sink (Sec. 4.3, reading R10): a block is a text block when its
+    token range overlaps the text range; expected sets worked out by hand
+    from the token ranges, including unaligned starts and ends."""
+    assert oracle.text_block_set(4096, block, *rng_) == expect
+
+
+def test_topk_count_fixed_values():
+    """Reading R9 at the long-video shape (NB = 862 key blocks of 128, two
+    text blocks): keep 5/10/20/50% give 44/87/173/431 blocks per video row
+    (ceil of 43.1, 86.2, 172.4 and 431.0); at block 64 (NB = 1,724, four text
+    blocks) keep 10% gives 173.  The clamps: nothing kept still keeps the text
+    blocks (or one block without text), everything kept is NB."""
+    assert [oracle.topk_count(b, 862, 2) for b in (500, 1000, 2000, 5000)] == [44, 87, 173, 431]
+    assert oracle.topk_count(1000, 1724, 4) == 173
+    assert oracle.topk_count(0, 862, 2) == 2
+    assert oracle.topk_count(0, 10, 0) == 1
+    assert oracle.topk_count(1, 862, 0) == 1            # ceil(0.0862)
+    assert oracle.topk_count(10000, 862, 2) == 862
+    assert oracle.topk_count(9999, 862, 2) == 862       # ceil(861.9138)
+    assert oracle.topk_count(100, 3, 5) == 5            # the text blocks win over the fraction
+
+
+def _two_block_heads(strengths, nb=10):
+    """Head h: every row p keeps mass a_h on blocks p and p+1 (mod nb) and 1
+    elsewhere, so its Recall at k = 1, 2, 3 ... is known by hand."""
+    W = np.ones((1, len(strengths), nb, nb), dtype=np.float32)
+    for h, a in enumerate(strengths):
+        for p in range(nb):
+            W[0, h, p, p] = a
+            W[0, h, p, (p + 1) % nb] = a
+    return W
+
+
+def test_hierarchical_cap_clamp_and_strict_threshold():
+    """Sec. 4.2 head-adaptive sparsity (reading R14), values worked out by
+    hand on heads whose Recall is known in closed form: with strengths a_h on
+    two blocks per row and 1 on the other eight, the Recall at k = 2 is
+    2a/(2a + 8).
+
+    * a = 100, 50, 20, 10 (Recall 0.96, 0.93, 0.83, 0.71 at base sparsity 0.8,
+      k = 2): all four exceed 0.5, so n = 4 is capped at floor(4/2) = 2; the
+      top two move to sparsity 0.9 (k = 1), the bottom two to 0.7 (k = 3).
+    * the same heads at base sparsity 0.2 (k = 8): (3s-1)/2 = -0.2 is clamped
+      to 0 (k = 10, every block), (1+s)/2 = 0.6 keeps 40% (k = 4).
+    * three heads (cap floor(3/2) = 1): only the top and bottom head move.
+    * "exceeds" is strict: a = 12 gives Recall exactly 24/32 = 0.75 at k = 2,
+      which does not exceed a threshold of 0.75 (n = 1 from a = 100 alone)."""
+    nb = 10
+    W = _two_block_heads([100, 50, 20, 10], nb)
+    sel = oracle.select_blocks(W, nb * 16, 16, 0, 0, "hierarchical", None,
+                               base_sparsity_bp=8000, recall_threshold_bp=5000)
+    assert sel["head_k"][0].tolist() == [1, 1, 3, 3]
+    sel = oracle.select_blocks(W, nb * 16, 16, 0, 0, "hierarchical", None,
+                               base_sparsity_bp=2000, recall_threshold_bp=5000)
+    assert sel["head_k"][0].tolist() == [4, 4, 10, 10]
+    W3 = _two_block_heads([20, 100, 10], nb)
+    sel = oracle.select_blocks(W3, nb * 16, 16, 0, 0, "hierarchical", None,
+                               base_sparsity_bp=8000, recall_threshold_bp=5000)
+    assert sel["head_k"][0].tolist() == [2, 1, 3]
+    Ws = _two_block_heads([100, 12, 12, 12], nb)
+    sel = oracle.select_blocks(Ws, nb * 16, 16, 0, 0, "hierarchical", None,
+                               base_sparsity_bp=8000, recall_threshold_bp=7500)
+    # n = 1: head 0 -> k = 1; the lowest Recall ties (0.75 each) go to the
+    # highest head index last in the ranking, so head 3 -> k = 3
+    assert sel["head_k"][0].tolist() == [1, 2, 2, 3]
+    assert float(sel["head_recall"][0, 1]) == 0.75
