@@ -133,9 +133,17 @@ def _check_qkv(*ts):
 
 
 def _select(mode: str, head_param_bp: Optional[Sequence[int]], text_sink: bool,
-            scores_given: bool, base_sparsity_bp: int = 8000, recall_threshold_bp: int = 8000):
-    m = {"topk": SELECT_TOPK, "coverage": SELECT_COVERAGE, "hierarchical": SELECT_HIERARCHICAL}[mode]
+            scores_given: bool, base_sparsity_bp: int = 8000, recall_threshold_bp: int = 8000,
+            heads: Optional[int] = None):
+    modes = {"topk": SELECT_TOPK, "coverage": SELECT_COVERAGE, "hierarchical": SELECT_HIERARCHICAL}
+    if mode not in modes:
+        raise AdaspaError(f"unknown selection mode {mode!r}")
+    m = modes[mode]
     params = list(head_param_bp) if head_param_bp is not None else []
+    # The library reads head_param_bp[0 .. H-1] in the per-head modes: a shorter
+    # list would be read past its end.
+    if m != SELECT_HIERARCHICAL and heads is not None and len(params) != heads:
+        raise AdaspaError(f"head_param_bp needs one entry per head ({heads}), got {len(params)}")
     arr = (ctypes.c_int32 * max(1, len(params)))(*[int(x) for x in params])
     ptr = ctypes.cast(arr, ctypes.POINTER(ctypes.c_int32)) if params else None
     flags = (F_TEXT_SINK if text_sink else 0) | (F_SCORES_GIVEN if scores_given else 0)
@@ -200,7 +208,7 @@ def block_search_workspace(shape, block, text_start, text_len, mode, head_param_
                            text_sink=True) -> int:
     B, H, L, D = shape
     prob = _problem_shape(B, H, L, D, block, text_start, text_len, None)
-    sel, _keep = _select(mode, head_param_bp, text_sink, False)
+    sel, _keep = _select(mode, head_param_bp, text_sink, False, heads=H)
     return int(load_library().adaspa_block_search_workspace(ctypes.byref(prob), ctypes.byref(sel)))
 
 
@@ -208,7 +216,7 @@ def block_search_capacity(shape, block, text_start, text_len, mode, head_param_b
                           text_sink=True) -> int:
     B, H, L, D = shape
     prob = _problem_shape(B, H, L, D, block, text_start, text_len, None)
-    sel, _keep = _select(mode, head_param_bp, text_sink, False)
+    sel, _keep = _select(mode, head_param_bp, text_sink, False, heads=H)
     return int(load_library().adaspa_block_search_capacity(ctypes.byref(prob), ctypes.byref(sel)))
 
 
@@ -237,7 +245,7 @@ def block_search(q, k, lse, *, block: int, text_start: int, text_len: int,
     nb = (L + block - 1) // block
     prob = _problem_shape(B, H, L, D, block, text_start, text_len, scale)
     sel, _keep = _select(mode, head_param_bp, text_sink, given, base_sparsity_bp,
-                         recall_threshold_bp)
+                         recall_threshold_bp, heads=H)
     cap = lib.adaspa_block_search_capacity(ctypes.byref(prob), ctypes.byref(sel))
     wsb = lib.adaspa_block_search_workspace(ctypes.byref(prob), ctypes.byref(sel))
     if cap < 0 or wsb == 0:

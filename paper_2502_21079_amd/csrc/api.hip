@@ -1,7 +1,6 @@
 // C ABI of libadaspa: argument validation on the host, then asynchronous
 // launches on the caller's stream.  No device memory is allocated here.
 #include <math.h>
-#include <stdlib.h>
 #include <string.h>
 
 #pragma GCC visibility push(default)
@@ -116,24 +115,6 @@ void hierarchical_counts(int s_bp, int nb, int n_text, int* k_base, int* k_hi, i
 
 }  // namespace
 
-namespace adaspa {
-// Work-to-XCD mapping (see the kernels): 1 gives each XCD one contiguous range
-// of (head, query tile) work items, so the workgroups sharing an L2 stream the
-// same K/V (dense attention and the mass pass: about 6x less HBM traffic than
-// hardware order); 0 keeps the hardware's round-robin order; 2 is the
-// head-chunked order; 3 (block-sparse attention) starts the text query blocks
-// first and then gives each XCD an equal contiguous share of every head, so
-// heads of different density stay balanced and neighbouring query blocks,
-// which select largely the same key blocks, share an L2.  ADASPA_XCD_MAP
-// overrides the per-kernel choice.
-int xcd_map_mode(int kernel_default) {
-  static const int env = [] {
-    const char* e = getenv("ADASPA_XCD_MAP");
-    return e ? atoi(e) : -1;
-  }();
-  return env >= 0 ? env : kernel_default;
-}
-}  // namespace adaspa
 
 #pragma GCC visibility push(default)
 extern "C" {
@@ -184,7 +165,6 @@ adaspa_status adaspa_dense_attn_lse(const adaspa_problem* prob, const void* q, c
   a.nkb = num_blocks(prob);
   a.scale = scale_of(prob);
   a.scale_log2 = a.scale * 1.4426950408889634f;
-  a.xcd_map = xcd_map_mode(1);
   a.claim = (uint32_t*)workspace;
   return launch_dense(a, prob->head_dim, (hipStream_t)stream) == hipSuccess ? ADASPA_OK : ADASPA_ERR_HIP;
 }
@@ -255,7 +235,6 @@ adaspa_status adaspa_block_search(const adaspa_problem* prob, const void* q, con
     m.block = prob->block;
     m.nkb = nb;
     m.scale_log2 = scale_of(prob) * 1.4426950408889634f;
-    m.xcd_map = xcd_map_mode(1);
     m.claim = (uint32_t*)((char*)workspace + wl.claim);
     if (launch_block_mass(m, prob->head_dim, s) != hipSuccess) return ADASPA_ERR_HIP;
   }
@@ -327,7 +306,6 @@ adaspa_status adaspa_block_sparse_attn(const adaspa_problem* prob, const void* q
   a.nkb = num_blocks(prob);
   a.scale = scale_of(prob);
   a.scale_log2 = a.scale * 1.4426950408889634f;
-  a.xcd_map = xcd_map_mode(3);
   a.claim = (uint32_t*)workspace;
   // Text query blocks keep every key block under the text sink, so they are
   // the longest rows; the kernel starts them first (the result does not

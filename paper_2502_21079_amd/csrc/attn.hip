@@ -77,10 +77,13 @@ __global__ __launch_bounds__(64 * NW, NW >= 8 ? 1 : 2) void attn_fwd_kernel(Attn
   const SlotPart<LD::ELEMS, 0> sK{sKV};
   const SlotPart<LD::ELEMS, LD::VOFF> sV{sKV};
 
+  // Work mapping.  Block-sparse: the text query blocks of every head first,
+  // then an equal contiguous share of every head's video query blocks per
+  // XCD (text_first_map).  Dense: one contiguous range of (head, query tile)
+  // items per XCD (xcd_remap), through the per-XCD queues when a workspace
+  // is given.
   int bh, qt;
-  if (a.xcd_map == 2) {
-    xcd_chunk_map(blockIdx.x, a.nqt, a.batch_heads, bh, qt);
-  } else if (SPARSE && (a.xcd_map == 1 || a.xcd_map == 3)) {
+  if constexpr (SPARSE) {
     int item = (int)blockIdx.x;
     if (item >= a.n_static) {                // the queued tail (see claim_item)
       __shared__ int s_tail;
@@ -89,18 +92,17 @@ __global__ __launch_bounds__(64 * NW, NW >= 8 ? 1 : 2) void attn_fwd_kernel(Attn
       item = s_tail;
       if (item < 0) return;
     }
-    text_first_map(item, a.n_items, a.nqt, a.tq0, a.tq1 - a.tq0, bh, qt, a.xcd_map == 3);
-  } else if (!SPARSE && a.claim != nullptr) {
-    __shared__ int s_item;
-    if (threadIdx.x == 0) s_item = claim_item(a.claim, 0, a.n_items);
-    __syncthreads();
-    const int item = s_item;
-    if (item < 0) return;                    // every item is taken
-    const int lid = a.xcd_map ? xcd_remap(item, a.n_items) : item;
-    bh = lid / a.nqt;
-    qt = lid % a.nqt;
+    text_first_map(item, a.n_items, a.nqt, a.tq0, a.tq1 - a.tq0, bh, qt);
   } else {
-    const int lid = a.xcd_map ? xcd_remap(blockIdx.x, a.n_wg) : (int)blockIdx.x;
+    int item = (int)blockIdx.x;
+    if (a.claim != nullptr) {
+      __shared__ int s_item;
+      if (threadIdx.x == 0) s_item = claim_item(a.claim, 0, a.n_items);
+      __syncthreads();
+      item = s_item;
+      if (item < 0) return;                  // every item is taken
+    }
+    const int lid = xcd_remap(item, a.n_items);
     bh = lid / a.nqt;
     qt = lid % a.nqt;
   }
@@ -325,6 +327,7 @@ __global__ __launch_bounds__(64 * NW, NW >= 8 ? 1 : 2) void attn_fwd_kernel(Attn
     }
     pv_tile<ND, VS>(sV[(nf - 1) & (RING - 1)] + voff, p_prev, o);
     lsum = finish_sums(rsum, bad, p_prev, hw, c32);
+    bad = bad || !acc_finite<ND>(o);
     redo = __any(bad);
     if (redo && lane == 0) s_redo = 1;
     __syncthreads();
@@ -440,7 +443,7 @@ __global__ __launch_bounds__(64 * NW, NW >= 8 ? 1 : 2) void attn_sparse_pair_ker
   const SlotPart<LD::ELEMS, LD::VOFF> sV{sKV};
 
   int bh, pq;
-  if (a.xcd_map == 1 || a.xcd_map == 3) {
+  {
     int item = (int)blockIdx.x;
     if (item >= a.n_static) {                // as in attn_fwd_kernel
       __shared__ int s_tail;
@@ -449,11 +452,7 @@ __global__ __launch_bounds__(64 * NW, NW >= 8 ? 1 : 2) void attn_sparse_pair_ker
       item = s_tail;
       if (item < 0) return;
     }
-    text_first_map(item, a.n_items, a.nqt, a.tq0, a.tq1 - a.tq0, bh, pq, a.xcd_map == 3);
-  } else {
-    const int lid = a.xcd_map ? xcd_remap(blockIdx.x, a.n_wg) : (int)blockIdx.x;
-    bh = lid / a.nqt;
-    pq = lid % a.nqt;
+    text_first_map(item, a.n_items, a.nqt, a.tq0, a.tq1 - a.tq0, bh, pq);
   }
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);   // wave-uniform
@@ -707,6 +706,7 @@ __global__ __launch_bounds__(64 * NW, NW >= 8 ? 1 : 2) void attn_sparse_pair_ker
     }
     pv_tile<ND, VS>(sV[(nf - 1) & 1] + voff, p_prev, o);
     lsum = finish_sums(rsum, bad, p_prev, hw, c32);
+    bad = bad || !acc_finite<ND>(o);
     redo = __any(bad);
     if (redo && lane == 0) s_redo = 1;
     __syncthreads();
@@ -814,20 +814,19 @@ __global__ __launch_bounds__(64 * NW, 2) void block_mass_kernel(MassParams a) {
   __shared__ float sW[QB][RING];    // blocks of the QB rows of W not yet written out
 
   const int ngrp = (a.nkb + QB - 1) / QB;    // query-block groups per head
+  // One contiguous range of (head, query-block group) items per XCD, through
+  // the per-XCD work queues when a workspace is given (see claim_item).
   int bh, pg;
-  if (a.xcd_map == 2) {
-    xcd_chunk_map(blockIdx.x, ngrp, a.batch_heads, bh, pg);
-  } else if (a.claim != nullptr) {           // per-XCD work queues (see claim_item)
-    __shared__ int s_item;
-    if (threadIdx.x == 0) s_item = claim_item(a.claim, 0, a.n_items);
-    __syncthreads();
-    const int item = s_item;
-    if (item < 0) return;
-    const int lid = a.xcd_map ? xcd_remap(item, a.n_items) : item;
-    bh = lid / ngrp;
-    pg = lid % ngrp;
-  } else {
-    const int lid = a.xcd_map ? xcd_remap(blockIdx.x, a.n_wg) : (int)blockIdx.x;
+  {
+    int item = (int)blockIdx.x;
+    if (a.claim != nullptr) {
+      __shared__ int s_item;
+      if (threadIdx.x == 0) s_item = claim_item(a.claim, 0, a.n_items);
+      __syncthreads();
+      item = s_item;
+      if (item < 0) return;
+    }
+    const int lid = xcd_remap(item, a.n_items);
     bh = lid / ngrp;
     pg = lid % ngrp;
   }
@@ -984,7 +983,6 @@ hipError_t launch_dense(AttnParams a, int D, hipStream_t st) {
   a.nqt = (a.seqlen + 255) / 256;
   a.n_items = a.nqt * a.batch_heads;
   a.n_wg = a.n_items;
-  if (a.xcd_map == 2) a.claim = nullptr;     // that mapping takes no items from the queues
   if (a.claim != nullptr) {
     // A quarter more workgroups than items: the XCDs that run ahead take the
     // items the others have not reached; surplus workgroups find every queue
@@ -1002,13 +1000,12 @@ hipError_t launch_dense(AttnParams a, int D, hipStream_t st) {
 // Work items of block-sparse attention: with a workspace, the first nine
 // tenths (rounded down to a multiple of 8) in the static order and the rest
 // claimed from the per-XCD queues, with half as many extra workgroups as
-// queued items (a fast XCD takes up to that many more than its share); the
-// queues serve only the mappings that name items (1 and 3).
+// queued items (a fast XCD takes up to that many more than its share).
 static hipError_t plan_sparse_items(AttnParams& a, hipStream_t st) {
   a.n_items = a.nqt * a.batch_heads;
   a.n_static = a.n_items;
   a.n_wg = a.n_items;
-  if (a.claim == nullptr || !(a.xcd_map == 1 || a.xcd_map == 3)) return hipSuccess;
+  if (a.claim == nullptr) return hipSuccess;
   a.n_static = (int)((int64_t)a.n_items * 9 / 10) / 8 * 8;
   a.n_wg = a.n_items + (a.n_items - a.n_static) / 2;
   hipLaunchKernelGGL(claim_reset_kernel, dim3(1), dim3(64), 0, st, a.claim);
@@ -1042,7 +1039,6 @@ template <int D, int QB, int NW>
 static hipError_t launch_mass_t(MassParams a, hipStream_t st) {
   a.n_items = (a.nkb + QB - 1) / QB * a.batch_heads;
   a.n_wg = a.n_items;
-  if (a.xcd_map == 2) a.claim = nullptr;     // as in launch_dense
   if (a.claim != nullptr) {                  // as in launch_dense
     a.n_wg = a.n_items + (a.n_items + 3) / 4;
     hipLaunchKernelGGL(claim_reset_kernel, dim3(1), dim3(64), 0, st, a.claim);

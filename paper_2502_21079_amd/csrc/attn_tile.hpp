@@ -430,6 +430,22 @@ __device__ __forceinline__ float finish_sums(RowSums& rsum, bool& bad, const bf1
   return hw == 0 ? v : 0.f;
 }
 
+// Whether every entry of the output accumulator is finite.  The row-sum test
+// bounds the probabilities, not their products with V: with large |V| a
+// product can overflow fp32 while the sums stay in range, so a non-finite
+// accumulator after the pipeline also sends the wave to the exact path (whose
+// tile-sum test keeps every probability below 2^16).  The maximum propagates
+// NaN, and the comparison fails for NaN and infinity.
+template <int ND>
+__device__ __forceinline__ bool acc_finite(const f32x16 (&o)[ND]) {
+  float m = 0.f;
+#pragma unroll
+  for (int d = 0; d < ND; ++d)
+#pragma unroll
+    for (int e = 0; e < 16; ++e) m = vmax(m, __builtin_fabsf(o[d][e]));
+  return m <= 3.4028234663852886e38f;
+}
+
 // Softmax of one tile outside the pipeline (masked tiles): P against the
 // current reference, moved first if this tile needs it.  Returns the factor
 // by which the output accumulator must be rescaled before this tile's P V

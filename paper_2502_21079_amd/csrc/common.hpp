@@ -44,30 +44,6 @@ __device__ __forceinline__ int xcd_remap(int bid, int n) {
   return off + k;
 }
 
-// Head-chunked mapping: each head's nqt tiles are cut into 8 contiguous
-// chunks and XCD x runs chunk x of every head, so every XCD works on a
-// contiguous run of query tiles (its L2 keeps the shared K/V) and on an equal
-// share of every head (heads of different cost stay balanced).  Tiles are
-// ordered (chunk, head, tile) and the round-robin dispatch share of XCD x is
-// a contiguous segment of that order, so the map is a bijection for any sizes.
-__device__ __forceinline__ void xcd_chunk_map(int bid, int nqt, int nbh, int& bh, int& qt) {
-  const int nx = 8, n = nqt * nbh;
-  const int q = n / nx, r = n % nx;
-  const int x = bid % nx, k = bid / nx;
-  const int idx = x * q + (x < r ? x : r) + k;        // position in (chunk, head, tile) order
-  // chunk c covers tiles [c*nqt/8, (c+1)*nqt/8) of every head
-  int c = 0, start = 0;
-  for (; c < nx - 1; ++c) {
-    const int sz = ((c + 1) * nqt) / nx - (c * nqt) / nx;
-    if (idx < start + sz * nbh) break;
-    start += sz * nbh;
-  }
-  const int c0 = (c * nqt) / nx, sz = ((c + 1) * nqt) / nx - c0;
-  const int rel = idx - start;
-  bh = rel / sz;
-  qt = c0 + rel % sz;
-}
-
 // Lane l's value and lane (l ^ 32)'s value, returned as (a, b) in an order
 // that depends on the half-wave: a = v[l & 31], b = v[(l & 31) + 32].  One
 // v_permlane32_swap (a VALU op; no LDS round trip as with a shuffle).
@@ -86,19 +62,19 @@ __device__ __forceinline__ float dpp_plus(float v) {
   const int moved = __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, v), CTRL, 0xF, 0xF, false);
   return v + __builtin_bit_cast(float, moved);
 }
-// Long rows first: the nt = ntq * nbh workgroups of the ntq query tiles
-// [tq0, tq0 + ntq) of every head are dispatched first (hardware ids 0..nt-1,
-// spread round-robin over the XCDs), and the other tiles follow with each XCD
-// receiving one contiguous range of the remaining (head, tile) order, as in
-// xcd_remap.  In block-sparse attention the text query blocks keep every key
-// block, so they are the longest rows by far; starting them first removes the
-// tail they would otherwise leave.  Bijective for any sizes.
-// With chunked, the other tiles follow in (chunk, head, tile) order instead,
-// chunk c holding tiles [c*m/8, (c+1)*m/8) of every head (m tiles per head),
-// so each XCD also receives an equal share of every head (heads of different
-// cost stay balanced) in contiguous runs.
+// Work order of block-sparse attention.  Long rows first: the nt = ntq * nbh
+// workgroups of the ntq query tiles [tq0, tq0 + ntq) of every head are
+// dispatched first (hardware ids 0..nt-1, spread round-robin over the XCDs);
+// in block-sparse attention the text query blocks keep every key block, so
+// they are the longest rows by far, and starting them first removes the tail
+// they would otherwise leave.  The other tiles follow in (chunk, head, tile)
+// order, chunk c holding tiles [c*m/8, (c+1)*m/8) of every head (m tiles per
+// head), and each XCD receives one contiguous range of that order: it works
+// on contiguous runs of query tiles, whose neighbours keep largely the same
+// key blocks (they share its L2), and on an equal share of every head (heads
+// of different cost stay balanced).  Bijective for any sizes.
 __device__ __forceinline__ void text_first_map(int hid, int n, int nqt, int tq0, int ntq, int& bh,
-                                               int& qt, bool chunked = false) {
+                                               int& qt) {
   const int nbh = n / nqt;
   const int nt = ntq * nbh;
   if (hid < nt) {
@@ -111,21 +87,15 @@ __device__ __forceinline__ void text_first_map(int hid, int n, int nqt, int tq0,
   int lid = cnt(hid, x) - cnt(nt, x);
   for (int y = 0; y < x; ++y) lid += cnt(n, y) - cnt(nt, y);
   const int nvq = nqt - ntq;
-  int r;
-  if (!chunked) {
-    bh = lid / nvq;
-    r = lid % nvq;
-  } else {
-    int c = 0, start = 0;
-    for (; c < 7; ++c) {
-      const int sz = ((c + 1) * nvq) / 8 - (c * nvq) / 8;
-      if (lid < start + sz * nbh) break;
-      start += sz * nbh;
-    }
-    const int c0 = (c * nvq) / 8, sz = ((c + 1) * nvq) / 8 - c0;
-    bh = (lid - start) / sz;
-    r = c0 + (lid - start) % sz;
+  int c = 0, start = 0;
+  for (; c < 7; ++c) {
+    const int sz = ((c + 1) * nvq) / 8 - (c * nvq) / 8;
+    if (lid < start + sz * nbh) break;
+    start += sz * nbh;
   }
+  const int c0 = (c * nvq) / 8, sz = ((c + 1) * nvq) / 8 - c0;
+  bh = (lid - start) / sz;
+  const int r = c0 + (lid - start) % sz;
   qt = r < tq0 ? r : r + ntq;
 }
 

@@ -25,8 +25,6 @@ struct AttnParams {
   int n_wg;                   // workgroups (set by the launcher)
   float scale;
   float scale_log2;           // scale * log2(e)
-  int xcd_map;                // 0 hardware order, 1 contiguous per XCD, 2 head-chunked,
-                              // 3 sparse: text first, then head-chunked
   int tq0, tq1;               // sparse: text query blocks [tq0, tq1), dispatched first
   int kb_guess, n_guess;      // sparse: first text block and the text block count (-1, 0: none),
                               // whose tiles every row begins with under the text sink
@@ -46,7 +44,6 @@ struct MassParams {
   int nkb;
   int n_wg;
   float scale_log2;
-  int xcd_map;
   uint32_t* claim;            // 8 work-queue counters (one per XCD), or null
   int n_items;                // with claim: work items (head, query-block group)
 };
@@ -82,9 +79,5 @@ hipError_t launch_dense(AttnParams a, int head_dim, hipStream_t st);
 hipError_t launch_sparse(AttnParams a, int head_dim, hipStream_t st);
 hipError_t launch_block_mass(MassParams a, int head_dim, hipStream_t st);
 hipError_t launch_select(const SelectParams& p, hipStream_t st);
-
-// Work-to-XCD mapping for the attention and mass kernels (0 hardware order,
-// 1 contiguous per XCD, 2 head-chunked); kernel_default unless overridden.
-int xcd_map_mode(int kernel_default);
 
 }  // namespace adaspa

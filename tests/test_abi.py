@@ -208,3 +208,18 @@ def test_binding_raises_without_library(monkeypatch, tmp_path):
     monkeypatch.setenv("ADASPA_LIB", str(tmp_path / "missing.so"))
     with pytest.raises(ad.AdaspaError):
         ad.load_library()
+
+
+def test_binding_checks_per_head_parameter_count(lib):
+    """The per-head modes read head_param_bp[0 .. H-1]: the binding refuses a
+    list of another length before it reaches the library."""
+    shape = (1, 24, 110336, 128)
+    with pytest.raises(ad.AdaspaError, match="one entry per head"):
+        ad.block_search_workspace(shape, 128, 0, 256, "topk", [9000])
+    with pytest.raises(ad.AdaspaError, match="one entry per head"):
+        ad.block_search_capacity(shape, 128, 0, 256, "coverage", [9000] * 25)
+    assert ad.block_search_capacity(shape, 128, 0, 256, "topk", [2000] * 24) > 0
+    # the hierarchical mode takes no per-head list
+    assert ad.block_search_capacity(shape, 128, 0, 256, "hierarchical", None) > 0
+    with pytest.raises(ad.AdaspaError, match="unknown selection mode"):
+        ad.block_search_capacity(shape, 128, 0, 256, "top-k", [2000] * 24)

@@ -1,5 +1,6 @@
 """The benchmarked chain at the long-video shape (B=1, H=24, L=110,336, d=128,
-block 128), in the launch configuration the benchmark times: dense attention
+block 128, and block 64, the paper's default, where NB = 1,724), in the
+launch configuration the benchmark times: dense attention
 + LSE, then the search with the fresh LSE (coverage 0.9 per head, text sink,
 caller workspace), then block-sparse attention with the text range given
 (text query blocks first, queued tail).
@@ -31,9 +32,14 @@ def inputs():
     return make_qkv(LONG, device="cuda")
 
 
+@pytest.fixture(scope="module", params=[128, 64], ids=["b128", "b64"])
+def wl(request):
+    return LONG if request.param == 128 else LONG.replace(block=64)
+
+
 @pytest.fixture(scope="module")
-def searched(inputs):
-    w = LONG
+def searched(inputs, wl):
+    w = wl
     B, H, L, D = w.batch, w.heads, w.seqlen, w.head_dim
     q, k, v = inputs
     tau = [w.coverage_bp] * H
@@ -46,9 +52,8 @@ def searched(inputs):
     return res
 
 
-def _oracle_masses(q, k, v, h, p):
+def _oracle_masses(w, q, k, v, h, p):
     """Oracle LSE of query block p of head h (all keys), then its block masses."""
-    w = LONG
     rows = np.arange(p * w.block, min((p + 1) * w.block, w.seqlen))
     idx = torch.as_tensor(rows, device=q.device)
     qr = f64(q[0, h, idx])
@@ -56,8 +61,8 @@ def _oracle_masses(q, k, v, h, p):
     return oracle.block_mass_rows(qr, f64(k[0, h]), l_ref, w.scale, w.block)
 
 
-def test_chain_masses_and_selection_sampled(inputs, searched):
-    w = LONG
+def test_chain_masses_and_selection_sampled(inputs, searched, wl):
+    w = wl
     q, k, v = inputs
     res = searched
     nb = w.nblocks
@@ -70,7 +75,7 @@ def test_chain_masses_and_selection_sampled(inputs, searched):
         kh = int(gk[0, h])
         assert len(tk) <= kh <= nb
         for p in sample_blocks(nb, 3, seed=900 + h, always=(0, 2)):
-            ref = _oracle_masses(q, k, v, h, p)
+            ref = _oracle_masses(w, q, k, v, h, p)
             check_mass(res.block_mass[0, h, p], ref, f"h{h} p{p}")
             r = h * nb + p
             got = ci[rp[r]:rp[r + 1]]
@@ -89,14 +94,16 @@ def test_chain_masses_and_selection_sampled(inputs, searched):
 
 
 @pytest.fixture(scope="module")
-def coverage_shaped_pattern():
+def coverage_shaped_pattern(wl):
     """Seeded lists shaped like the coverage-0.9 pattern at this shape: text
     query blocks keep every block, video query blocks keep the text blocks
-    plus a per-head number of others (15 to 60 blocks per row)."""
-    w = LONG
+    plus a per-head number of others (15 to 60 blocks of 128 per row, twice
+    as many blocks of 64)."""
+    w = wl
     nb = w.nblocks
     tb = text_blocks(w.seqlen, w.block, w.text_start, w.text_len)
-    counts = np.random.default_rng(31).integers(15, 61, size=w.heads)
+    f = 128 // w.block
+    counts = np.random.default_rng(31).integers(15 * f, 60 * f + 1, size=w.heads)
     rows = []
     for h in range(w.heads):
         rp_h, ci_h = random_block_lists(nb, nb, int(counts[h]), seed=3100 + h, always=tb)
@@ -108,8 +115,8 @@ def coverage_shaped_pattern():
     return row_ptr, col_idx
 
 
-def test_sparse_coverage_shaped_as_benchmarked(inputs, coverage_shaped_pattern):
-    w = LONG
+def test_sparse_coverage_shaped_as_benchmarked(inputs, coverage_shaped_pattern, wl):
+    w = wl
     q, k, v = inputs
     nb = w.nblocks
     rpn, cin = coverage_shaped_pattern
@@ -119,7 +126,7 @@ def test_sparse_coverage_shaped_as_benchmarked(inputs, coverage_shaped_pattern):
                                     text_len=w.text_len)
     torch.cuda.synchronize()
     for h in HEADS:
-        blocks = sample_blocks(nb, 4, seed=950 + h, always=(0, 1, 2))
+        blocks = sample_blocks(nb, 4, seed=950 + h, always=(0, 1, 2, 3, 4))
         o_ref, l_ref = oracle.block_sparse_attention(f64(q[0, h]), f64(k[0, h]), f64(v[0, h]),
                                                      rpn[h * nb:(h + 1) * nb + 1], cin, w.scale,
                                                      w.block, qblocks=blocks)

@@ -80,3 +80,43 @@ def test_mass_extreme_scores(kind, D, block, L):
     for h in range(2):
         ref = oracle.block_mass(f64(q[0, h]), f64(k[0, h]), f64(lse[0, h]), scale, block)
         check_mass(res.block_mass[0, h], ref, f"{kind} h{h}")
+
+
+BIG_V = 2.0 ** 72
+
+
+@pytest.mark.parametrize("kind", ["rising", "spiky"])
+@pytest.mark.parametrize("block", [64, 128])
+def test_large_values_take_the_exact_path(kind, block):
+    """Large |V|.  The lazy softmax reference lets a tile's probabilities grow
+    to about 2^58 before the row sums move it; times V entries near 2^74 the
+    products overflow fp32 in the output accumulator while the row sums stay
+    in range.  Those rows must be redone on the exact path.  V is the N(0, 1)
+    draw scaled by 2^72 (exact in bf16); outputs divided by 2^72 are checked
+    against the oracle on the unscaled V, for dense, block-sparse and the
+    all-blocks identity."""
+    L, D = 1000, 64
+    (q, k, v0), scale = make_extreme_qkv(kind, heads=2, seqlen=L, head_dim=D, device="cuda")
+    v = (v0.float() * BIG_V).to(torch.bfloat16)
+    assert torch.equal(v.float() / BIG_V, v0.float())
+    nb = (L + block - 1) // block
+    od, ld = ad.dense_attn_lse(q, k, v, scale=scale)
+    rp, ci = random_block_lists(2 * nb, nb, 5, seed=91 + block, always=[0])
+    os_, ls = ad.block_sparse_attn(q, k, v, rp.cuda(), ci.cuda(), block=block, scale=scale,
+                                   text_start=0, text_len=0)
+    rpa = (torch.arange(2 * nb + 1, dtype=torch.int32) * nb).cuda()
+    cia = torch.arange(nb, dtype=torch.int32).repeat(2 * nb).cuda()
+    oa, la = ad.block_sparse_attn(q, k, v, rpa, cia, block=block, scale=scale, text_start=0,
+                                  text_len=0)
+    torch.cuda.synchronize()
+    assert torch.equal(od, oa) and torch.equal(ld, la)
+    rpn, cin = rp.numpy(), ci.numpy()
+    for h in range(2):
+        qh, kh, vh = f64(q[0, h]), f64(k[0, h]), f64(v0[0, h])
+        o_ref, l_ref = oracle.dense_attention(qh, kh, vh, scale)
+        check_out(od[0, h].float() / BIG_V, o_ref, f"{kind} dense h{h}")
+        check_lse(ld[0, h], l_ref, f"{kind} dense lse h{h}")
+        o_sp, l_sp = oracle.block_sparse_attention(qh, kh, vh, rpn[h * nb:(h + 1) * nb + 1], cin,
+                                                   scale, block)
+        check_out(os_[0, h].float() / BIG_V, o_sp, f"{kind} b{block} sparse h{h}")
+        check_lse(ls[0, h], l_sp, f"{kind} b{block} sparse lse h{h}")
