@@ -417,9 +417,15 @@ __global__ __launch_bounds__(64 * NW, NW >= 8 ? 1 : 2) void attn_fwd_kernel(Attn
 // Four waves cover query blocks 2P (waves 0-1) and 2P+1 (waves 2-3), 128
 // rows, and walk the sorted union of the two rows' key-block lists through
 // the same pipeline as attn_fwd_kernel (one 64-key tile per block).  For a
-// tile that only one row keeps, the other half's scores are set to -inf, so
-// its probabilities are exact zeros: each half accumulates exactly its own
-// tiles, in ascending order, as a one-block workgroup would.  Neighbouring
+// tile that only one row keeps, the other half takes its probabilities
+// against a reference of +inf, so they are exact zeros (exp2(-inf)) and each
+// half accumulates exactly its own tiles, in ascending order, as a one-block
+// workgroup would; that costs one scalar select per step (overwriting the
+// scores with -inf made every step wait for its score MFMAs, ~7%).  A
+// non-finite score in such a tile (an inf or NaN in a key the half does not
+// keep) would still reach the half's sums; it leaves them, or the output
+// accumulator, non-finite, which sends the wave to the exact path, where the
+// tile's scores are masked to -inf before the softmax.  Neighbouring
 // query blocks keep mostly the same key blocks, so the union is little larger
 // than each list, and every tile brought into LDS serves 128 rows.  Rows
 // must be strictly ascending lists of blocks in [0, NB); otherwise (or for
@@ -623,7 +629,7 @@ __global__ __launch_bounds__(64 * NW, NW >= 8 ? 1 : 2) void attn_sparse_pair_ker
     __syncthreads();
     f32x16 s_cur[2];
     qk_tile<D, KS>(sK[0], qf, c32, hw, s_cur);
-    if (!(uk[0] & mybit)) hide(s_cur);
+    bool hid = !(uk[0] & mybit);
     __syncthreads();                  // sK[0] is refilled by step 0
 
     bf16x8 p_prev[2][2];
@@ -672,15 +678,15 @@ __global__ __launch_bounds__(64 * NW, NW >= 8 ? 1 : 2) void attn_sparse_pair_ker
       f32x16 s_next[2];
       bf16x8 p_cur[2][2];
       pipelined_step<D, KS, VS>(loads, rdK + klane, rdV + voff, qf, s_cur, p_prev, s_next, p_cur, o, sl2,
-                                ref.mc, rsum);
-      move_reference(ref, rsum, bad, s_cur, p_cur, pend, pend_alpha, sl2, c32);
+                                hid ? INFINITY : ref.mc, rsum);
+      move_reference(ref, rsum, bad, s_cur, p_cur, pend, pend_alpha, sl2, c32, hid);
 #pragma unroll
       for (int g = 0; g < 2; ++g) {
         s_cur[g] = s_next[g];
 #pragma unroll
         for (int s2 = 0; s2 < 2; ++s2) p_prev[g][s2] = p_cur[g][s2];
       }
-      if (!(pick(uk, (t + 1) / SUB - u0) & mybit)) hide(s_cur);   // scores of tile t+1
+      hid = !(pick(uk, (t + 1) / SUB - u0) & mybit);   // tile t+1
       if ((t + 1) % SUB == 0) {          // tile t was the last of entry u0
         ub[0] = ub[1];
         uk[0] = uk[1];

@@ -392,10 +392,13 @@ __device__ __forceinline__ float exp_tile(const f32x16 (&s)[2], float sl2, float
 // reference yet take this tile's maximum (their sums so far are 0).  The sums
 // are rescaled here, the output accumulator at the start of the next step
 // (pend), and the current tile's probabilities are taken again against the
-// new reference.  bad is set when a sum has left the safe range.
+// new reference.  bad is set when a sum has left the safe range.  A hidden
+// tile (block-64 pairs: one the other query block keeps) never sets the
+// reference and its probabilities stay exact zeros.
 __device__ __forceinline__ void move_reference(RowRef& ref, RowSums& rsum, bool& bad,
                                                const f32x16 (&s_cur)[2], bf16x8 (&p_cur)[2][2],
-                                               bool& pend, float& pend_alpha, float sl2, int c32) {
+                                               bool& pend, float& pend_alpha, float sl2, int c32,
+                                               bool hidden = false) {
   const float sr = rsum.acc[0];
   if (!__any(ref.m == -INFINITY || sr > kRowSumLimit)) return;
   bad = bad || !(sr <= kRowSumBad);
@@ -406,14 +409,14 @@ __device__ __forceinline__ void move_reference(RowRef& ref, RowSums& rsum, bool&
   const float d = RowSums::for_row(dr, c32);        // the same value for this lane's row
   float al;
   if (ref.m == -INFINITY) {
-    al = ref.raise(s_cur, sl2);
+    al = hidden ? 1.f : ref.raise(s_cur, sl2);
   } else {
     if (d > 0.f) ref.shift(d, sl2);
     al = fast_exp2(-d);
   }
   pend_alpha = al;
   pend = true;
-  exp_tile(s_cur, sl2, ref.mc, p_cur);
+  exp_tile(s_cur, sl2, hidden ? INFINITY : ref.mc, p_cur);
 }
 
 // After the last pipelined tile: its probabilities join the sums, a sum out

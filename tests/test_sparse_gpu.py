@@ -215,3 +215,36 @@ def test_sparse_moderate_sampled():
         idx = torch.as_tensor(rows, device="cuda")
         check_out(out[0, h, idx], o_ref, f"h{h}")
         check_lse(lse[0, h, idx], l_ref)
+
+
+@pytest.mark.parametrize("bad", [float("nan"), float("inf")])
+def test_nonfinite_key_in_a_block_only_the_partner_keeps(bad):
+    """Block 64 pairs two query blocks over the union of their lists.  A
+    non-finite key in a block that only one of the two keeps must not reach
+    the other: its rows match the oracle, which never looks at that block;
+    the rows that keep it are non-finite, as in the oracle."""
+    w = TINY                                   # 32 blocks of 64
+    q, k, v = make_qkv(w, device="cuda")
+    nb = w.nblocks
+    k[0, :, 20 * 64 + 7, :] = bad              # a key of block 20, both heads
+    lists = [[0, 3 * (p % 5) + 1] if p % 2 else sorted({0, 3 * (p % 5) + 1, 9}) for p in range(nb)]
+    lists[2] = [0, 5, 20]                      # pair (2, 3): only block 2 keeps block 20
+    lists[3] = [0, 5, 9]
+    lists[10] = [0, 12]                        # pair (10, 11): only block 11 keeps block 20
+    lists[11] = [0, 12, 20, 21]
+    all_lists = lists * w.heads
+    rp = torch.tensor([0] + list(np.cumsum([len(x) for x in all_lists])), dtype=torch.int32)
+    ci = torch.tensor([c for x in all_lists for c in x], dtype=torch.int32)
+    out, lse = ad.block_sparse_attn(q, k, v, rp.cuda(), ci.cuda(), block=64)
+    torch.cuda.synchronize()
+    for h in range(w.heads):
+        qh, kh, vh = f64(q[0, h]), f64(k[0, h]), f64(v[0, h])
+        for p, kept in enumerate(lists):
+            rows = slice(p * 64, (p + 1) * 64)
+            if 20 in kept:
+                assert not torch.isfinite(out[0, h, rows].float()).all(), (h, p)
+                continue
+            mask = oracle.key_mask_from_blocks(kept, w.seqlen, 64)
+            o_ref, l_ref = oracle.masked_attention(qh[rows], kh, vh, mask, w.scale)
+            check_out(out[0, h, rows], o_ref, f"h{h} p{p}")
+            check_lse(lse[0, h, rows], l_ref, f"h{h} p{p}")
