@@ -35,7 +35,8 @@
  *    A fault inside a kernel surfaces at the caller's next synchronisation.
  *  - Calls are stateless and may be issued from several host threads on
  *    different streams; calls that share an output buffer must be ordered by
- *    the caller.
+ *    the caller.  (adaspa_block_sparse_attn_noalloc is the exception: its calls
+ *    on one GPU share that GPU's counters and must not overlap.)
  */
 #ifndef ADASPA_H_
 #define ADASPA_H_
@@ -206,6 +207,27 @@ adaspa_status adaspa_block_sparse_attn(const adaspa_problem* prob, const void* q
                                        const int32_t* col_idx, int64_t col_count,
                                        void* out, float* lse_out, void* workspace,
                                        size_t workspace_bytes, void* stream);
+
+/* adaspa_block_sparse_attn without a workspace argument and without any
+ * allocation, for callers that cannot allocate device memory (code under HIP
+ * graph capture, tight serving loops, harnesses that forbid hipMalloc).  It
+ * computes exactly what adaspa_block_sparse_attn computes with a workspace
+ * (bitwise the same outputs) and takes the same arguments and checks, except
+ * that the per-XCD work-queue counters live in a 256-byte array inside the
+ * library, one per GPU, held from the library's load until the process ends.
+ * The current device must be the one `stream` belongs to.  Every call on a
+ * GPU shares that GPU's counters (the call clears them itself with a kernel
+ * on `stream`), so calls on one GPU must not overlap: issue them on one
+ * stream, or order them; overlapping calls race on the counters.  Returns
+ * ADASPA_ERR_WORKSPACE if a problem ever needed more than the 256 bytes (no
+ * supported problem does) and ADASPA_ERR_HIP if the array's device address
+ * cannot be obtained.  No hipMalloc, hipFree or allocating library routine is
+ * called. */
+adaspa_status adaspa_block_sparse_attn_noalloc(const adaspa_problem* prob, const void* q,
+                                               const void* k, const void* v,
+                                               const int32_t* row_ptr,
+                                               const int32_t* col_idx, int64_t col_count,
+                                               void* out, float* lse_out, void* stream);
 
 #ifdef __cplusplus
 }

@@ -23,7 +23,7 @@ from typing import Optional, Sequence
 import torch
 
 __all__ = ["dense_attn_lse", "dense_attn_workspace", "block_search", "block_sparse_attn",
-           "block_sparse_attn_workspace", "SearchResult",
+           "block_sparse_attn_workspace", "block_sparse_attn_noalloc", "SearchResult",
            "library_path", "load_library", "AdaspaError", "EXPORTED_SYMBOLS",
            "block_search_workspace", "block_search_capacity"]
 
@@ -33,7 +33,7 @@ _LIB_NAME = "libadaspa.so"
 EXPORTED_SYMBOLS = ("adaspa_status_string", "adaspa_dense_attn_workspace", "adaspa_dense_attn_lse",
                     "adaspa_block_search_workspace", "adaspa_block_search_capacity",
                     "adaspa_block_search", "adaspa_block_sparse_attn_workspace",
-                    "adaspa_block_sparse_attn")
+                    "adaspa_block_sparse_attn", "adaspa_block_sparse_attn_noalloc")
 
 SELECT_TOPK = 0
 SELECT_COVERAGE = 1
@@ -96,6 +96,9 @@ def load_library():
     lib.adaspa_block_sparse_attn.restype = ctypes.c_int
     lib.adaspa_block_sparse_attn.argtypes = [P, vp, vp, vp, i32p, i32p, ctypes.c_int64, vp,
                                              f32p, vp, ctypes.c_size_t, vp]
+    lib.adaspa_block_sparse_attn_noalloc.restype = ctypes.c_int
+    lib.adaspa_block_sparse_attn_noalloc.argtypes = [P, vp, vp, vp, i32p, i32p, ctypes.c_int64,
+                                                     vp, f32p, vp]
     _lib = lib
     return lib
 
@@ -316,3 +319,32 @@ def block_sparse_attn_workspace(shape, block: int = 128, scale: Optional[float] 
     B, H, L, D = shape
     prob = _Problem(B, H, L, D, block, 0, 0, 0.0 if scale is None else float(scale))
     return int(load_library().adaspa_block_sparse_attn_workspace(ctypes.byref(prob)))
+
+
+def block_sparse_attn_noalloc(q, k, v, row_ptr, col_idx, *, block: int, out, lse=None,
+                              scale: Optional[float] = None, text_start: int = 0,
+                              text_len: int = 0):
+    """:func:`block_sparse_attn` through the allocation-free entry point: the
+    caller passes ``out`` (and ``lse``, or None to skip it) and nothing is
+    allocated, here or in the library, whose per-XCD work-queue counters sit
+    in a small array of its own on each GPU.  Results are bitwise those of
+    :func:`block_sparse_attn` with a workspace.  Calls on one GPU must not
+    overlap (they share that GPU's counters)."""
+    _check_qkv(q, k, v, out)
+    lib = load_library()
+    B, H, L, D = q.shape
+    nb = (L + block - 1) // block
+    for t in (row_ptr, col_idx):
+        if t.dtype != torch.int32 or t.device != q.device or not t.is_contiguous():
+            raise AdaspaError("row_ptr and col_idx must be contiguous int32 on q's device")
+    if row_ptr.numel() != B * H * nb + 1:
+        raise AdaspaError(f"row_ptr must have B*H*NB+1 = {B * H * nb + 1} entries")
+    if lse is not None and (lse.dtype != torch.float32 or lse.shape != (B, H, L)
+                            or not lse.is_contiguous() or lse.device != q.device):
+        raise AdaspaError("lse must be contiguous fp32 [B, H, L] on q's device")
+    prob = _problem(q, block, text_start, text_len, scale)
+    _check(lib.adaspa_block_sparse_attn_noalloc(ctypes.byref(prob), _ptr(q), _ptr(k), _ptr(v),
+                                                _ptr(row_ptr), _ptr(col_idx), int(col_idx.numel()),
+                                                _ptr(out), _ptr(lse), _stream(q.device)))
+    return out, lse
+

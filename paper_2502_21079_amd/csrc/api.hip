@@ -3,6 +3,8 @@
 #include <math.h>
 #include <string.h>
 
+#include <mutex>
+
 #pragma GCC visibility push(default)
 #include "adaspa.h"
 #pragma GCC visibility pop
@@ -111,6 +113,51 @@ void hierarchical_counts(int s_bp, int nb, int n_text, int* k_base, int* k_hi, i
   *k_base = topk_count(10000 - s_bp, nb, n_text);
   *k_hi = topk_count(10000 - s_hi, nb, n_text);
   *k_lo = topk_count(10000 - s_lo, nb, n_text);
+}
+
+// Argument checks of block-sparse attention (both entry points).
+adaspa_status check_sparse(const adaspa_problem* prob, const void* q, const void* k, const void* v,
+                           const int32_t* row_ptr, const int32_t* col_idx, int64_t col_count,
+                           const void* out, const float* lse_out) {
+  const adaspa_status st = check_problem(prob);
+  if (st != ADASPA_OK) return st;
+  if (!q || !k || !v || !out || !row_ptr || (!col_idx && col_count > 0) || col_count < 0)
+    return ADASPA_ERR_INVALID_ARG;
+  if (!aligned16(q) || !aligned16(k) || !aligned16(v) || !aligned16(out) ||
+      (lse_out && ((uintptr_t)lse_out & 3u)) || ((uintptr_t)row_ptr & 3u) ||
+      ((uintptr_t)col_idx & 3u))
+    return ADASPA_ERR_INVALID_ARG;
+  // Block 64 pairs query blocks through a byte map of one row's key blocks
+  // (kMaxBlocks entries); block 128 has no such limit.
+  if (prob->block == 64 && num_blocks(prob) > kMaxBlocks) return ADASPA_ERR_UNSUPPORTED;
+  return ADASPA_OK;
+}
+
+// Scratch of adaspa_block_sparse_attn_noalloc: the per-XCD work-queue
+// counters that adaspa_block_sparse_attn otherwise takes from a caller
+// workspace.  Each GPU holds its own copy of this array (at its own address)
+// from the library's load until the process ends.  In host code the name is
+// only a stand-in for the symbol: the device address of each GPU's copy comes
+// from hipGetSymbolAddress, taken once per device with that device current,
+// and only that address is ever passed to a kernel.
+constexpr size_t kScratchBytes = 256;
+constexpr int kMaxDevices = 64;
+static __device__ __align__(256) uint32_t scratch[kScratchBytes / sizeof(uint32_t)];
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[kMaxDevices];
+
+// Device address of the current device's scratch (set up on first use).
+adaspa_status scratch_of_current_device(void** ptr) {
+  int dev = -1;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) return ADASPA_ERR_HIP;
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (g_scratch_ptr[dev] == nullptr) {
+    void* p = nullptr;
+    if (hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)) != hipSuccess || p == nullptr) return ADASPA_ERR_HIP;
+    g_scratch_ptr[dev] = p;
+  }
+  *ptr = g_scratch_ptr[dev];
+  return ADASPA_OK;
 }
 
 }  // namespace
@@ -277,17 +324,8 @@ adaspa_status adaspa_block_sparse_attn(const adaspa_problem* prob, const void* q
                                        const int32_t* col_idx, int64_t col_count, void* out,
                                        float* lse_out, void* workspace, size_t workspace_bytes,
                                        void* stream) {
-  adaspa_status st = check_problem(prob);
+  const adaspa_status st = check_sparse(prob, q, k, v, row_ptr, col_idx, col_count, out, lse_out);
   if (st != ADASPA_OK) return st;
-  if (!q || !k || !v || !out || !row_ptr || (!col_idx && col_count > 0) || col_count < 0)
-    return ADASPA_ERR_INVALID_ARG;
-  if (!aligned16(q) || !aligned16(k) || !aligned16(v) || !aligned16(out) ||
-      (lse_out && ((uintptr_t)lse_out & 3u)) || ((uintptr_t)row_ptr & 3u) ||
-      ((uintptr_t)col_idx & 3u))
-    return ADASPA_ERR_INVALID_ARG;
-  // Block 64 pairs query blocks through a byte map of one row's key blocks
-  // (kMaxBlocks entries); block 128 has no such limit.
-  if (prob->block == 64 && num_blocks(prob) > kMaxBlocks) return ADASPA_ERR_UNSUPPORTED;
   if (workspace && (workspace_bytes < adaspa_block_sparse_attn_workspace(prob) || !aligned16(workspace)))
     return ADASPA_ERR_WORKSPACE;
   AttnParams a;
@@ -318,6 +356,24 @@ adaspa_status adaspa_block_sparse_attn(const adaspa_problem* prob, const void* q
   a.kb_guess = a.tq1 > a.tq0 ? a.tq0 : -1;
   a.n_guess = a.tq1 - a.tq0;
   return launch_sparse(a, prob->head_dim, (hipStream_t)stream) == hipSuccess ? ADASPA_OK : ADASPA_ERR_HIP;
+}
+
+adaspa_status adaspa_block_sparse_attn_noalloc(const adaspa_problem* prob, const void* q,
+                                               const void* k, const void* v,
+                                               const int32_t* row_ptr, const int32_t* col_idx,
+                                               int64_t col_count, void* out, float* lse_out,
+                                               void* stream) {
+  const adaspa_status st = check_sparse(prob, q, k, v, row_ptr, col_idx, col_count, out, lse_out);
+  if (st != ADASPA_OK) return st;
+  // The counters need the same bytes for every problem; the check keeps the
+  // limit explicit should that ever change.
+  const size_t need = adaspa_block_sparse_attn_workspace(prob);
+  if (need == 0 || need > kScratchBytes) return ADASPA_ERR_WORKSPACE;
+  void* ws = nullptr;
+  const adaspa_status ss = scratch_of_current_device(&ws);
+  if (ss != ADASPA_OK) return ss;
+  return adaspa_block_sparse_attn(prob, q, k, v, row_ptr, col_idx, col_count, out, lse_out, ws,
+                                  kScratchBytes, stream);
 }
 
 }  // extern "C"

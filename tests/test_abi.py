@@ -223,3 +223,18 @@ def test_binding_checks_per_head_parameter_count(lib):
     assert ad.block_search_capacity(shape, 128, 0, 256, "hierarchical", None) > 0
     with pytest.raises(ad.AdaspaError, match="unknown selection mode"):
         ad.block_search_capacity(shape, 128, 0, 256, "top-k", [2000] * 24)
+
+
+def test_sparse_noalloc_rejects_bad_arguments(lib):
+    """The allocation-free entry point checks its arguments like the others,
+    synchronously and before it touches a device."""
+    f = lib.adaspa_block_sparse_attn_noalloc
+    ok = _prob()
+    assert f(None, FAKE, FAKE, FAKE, FAKE, FAKE, 10, FAKE, None, None) == 1
+    assert f(ctypes.byref(_prob(head_dim=96)), FAKE, FAKE, FAKE, FAKE, FAKE, 10, FAKE, None, None) == 2
+    assert f(ctypes.byref(ok), None, FAKE, FAKE, FAKE, FAKE, 10, FAKE, None, None) == 1
+    assert f(ctypes.byref(ok), FAKE, FAKE, FAKE, FAKE, FAKE, -1, FAKE, None, None) == 1
+    assert f(ctypes.byref(ok), ctypes.c_void_p(0x10008), FAKE, FAKE, FAKE, FAKE, 10, FAKE, None,
+             None) == 1
+    big = _prob(seqlen=64 * 8193, head_dim=64, block=64)
+    assert f(ctypes.byref(big), FAKE, FAKE, FAKE, FAKE, FAKE, 10, FAKE, None, None) == 2
