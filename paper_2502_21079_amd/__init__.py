@@ -227,13 +227,15 @@ def block_search(q, k, lse, *, block: int, text_start: int, text_len: int,
                  mode: str, head_param_bp: Optional[Sequence[int]] = None, text_sink: bool = True,
                  scale: Optional[float] = None, scores: Optional[torch.Tensor] = None,
                  shape=None, workspace: Optional[torch.Tensor] = None,
-                 base_sparsity_bp: int = 8000, recall_threshold_bp: int = 8000) -> SearchResult:
+                 base_sparsity_bp: int = 8000, recall_threshold_bp: int = 8000,
+                 result: Optional["SearchResult"] = None) -> SearchResult:
     """Block masses W_sum_attn from ``lse`` (fresh or cached) and the per-head
     selection.  ``mode`` is "topk" or "coverage" (per-head ``head_param_bp``)
     or "hierarchical" (``base_sparsity_bp``, ``recall_threshold_bp``, Sec. 4.2).
     With ``scores`` given (fp32 [B, H, NB, NB]) the mass pass is skipped and
     those masses are selected from (then q, k, lse may be None and ``shape`` =
-    (B, H, L, D) is required)."""
+    (B, H, L, D) is required).  ``result`` (an earlier SearchResult of the same
+    problem and selection) is filled in place instead of new outputs."""
     lib = load_library()
     given = scores is not None
     if given:
@@ -255,16 +257,25 @@ def block_search(q, k, lse, *, block: int, text_start: int, text_len: int,
         _check(lib.adaspa_block_search(ctypes.byref(prob), None, None, None, ctypes.byref(sel),
                                        None, None, None, 0, None, None, None, 0, None))
         raise AdaspaError("invalid block_search arguments")
-    if given:
-        if scores.dtype != torch.float32 or scores.shape != (B, H, nb, nb) or not scores.is_contiguous():
-            raise AdaspaError("scores must be contiguous fp32 [B, H, NB, NB]")
-        mass = scores
+    if result is not None:
+        ok = (result.block_mass.shape == (B, H, nb, nb) and result.row_ptr.numel() == B * H * nb + 1
+              and result.col_idx.numel() >= cap and result.head_k.shape == (B, H)
+              and result.block_mass.device == dev and not given)
+        if not ok:
+            raise AdaspaError("result does not fit this search (shape, capacity or device)")
+        mass, row_ptr, col_idx = result.block_mass, result.row_ptr, result.col_idx
+        head_k, head_recall = result.head_k, result.head_recall
     else:
-        mass = torch.empty(B, H, nb, nb, dtype=torch.float32, device=dev)
-    row_ptr = torch.empty(B * H * nb + 1, dtype=torch.int32, device=dev)
-    col_idx = torch.empty(max(int(cap), 1), dtype=torch.int32, device=dev)
-    head_k = torch.empty(B, H, dtype=torch.int32, device=dev)
-    head_recall = torch.empty(B, H, dtype=torch.float32, device=dev)
+        if given:
+            if scores.dtype != torch.float32 or scores.shape != (B, H, nb, nb) or not scores.is_contiguous():
+                raise AdaspaError("scores must be contiguous fp32 [B, H, NB, NB]")
+            mass = scores
+        else:
+            mass = torch.empty(B, H, nb, nb, dtype=torch.float32, device=dev)
+        row_ptr = torch.empty(B * H * nb + 1, dtype=torch.int32, device=dev)
+        col_idx = torch.empty(max(int(cap), 1), dtype=torch.int32, device=dev)
+        head_k = torch.empty(B, H, dtype=torch.int32, device=dev)
+        head_recall = torch.empty(B, H, dtype=torch.float32, device=dev)
     if workspace is None or workspace.numel() < wsb:
         workspace = torch.empty(int(wsb), dtype=torch.uint8, device=dev)
     _check(lib.adaspa_block_search(ctypes.byref(prob), _ptr(q), _ptr(k), _ptr(lse),

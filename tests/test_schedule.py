@@ -1,0 +1,38 @@
+"""Host logic of the two-phase search schedule (overview figure; Sec. 4.2,
+Fused LSE-Cached Online Search; Sec. 5 defaults T_s = {10, 30} after ten
+full-attention steps).  No GPU needed."""
+import pytest
+
+from paper_2502_21079_amd import AdaspaError
+from paper_2502_21079_amd.schedule import (CACHED_SEARCH, DENSE, FUSED_SEARCH, SPARSE,
+                                           SearchSchedule)
+
+
+def test_paper_default_schedule():
+    s = SearchSchedule((10, 30))
+    acts = [s.action(t) for t in range(50)]
+    assert acts[:10] == [DENSE] * 10                  # ten warm-up steps at full attention
+    assert acts[10] == FUSED_SEARCH
+    assert acts[11:30] == [SPARSE] * 19
+    assert acts[30] == CACHED_SEARCH
+    assert acts[31:] == [SPARSE] * 19
+    assert s.warmup == 10
+    assert [s.pattern_step(t) for t in (0, 9, 10, 11, 29, 30, 31, 49)] == \
+        [None, None, None, 10, 10, 30, 30, 30]
+
+
+def test_no_warmup_and_single_search():
+    s = SearchSchedule((0, 30))                       # the paper's length-scaling setting
+    assert s.action(0) == FUSED_SEARCH and s.action(1) == SPARSE and s.action(30) == CACHED_SEARCH
+    s1 = SearchSchedule((0,))                         # search once, reuse for every later step
+    assert [s1.action(t) for t in range(4)] == [FUSED_SEARCH, SPARSE, SPARSE, SPARSE]
+    s3 = SearchSchedule((30, 5, 5, 20))               # sorted, duplicates dropped
+    assert s3.search_steps == (5, 20, 30)
+    assert [s3.action(t) for t in (4, 5, 6, 20, 30)] == [DENSE, FUSED_SEARCH, SPARSE,
+                                                          CACHED_SEARCH, CACHED_SEARCH]
+
+
+@pytest.mark.parametrize("bad", [(), (-1, 4)])
+def test_invalid_schedules(bad):
+    with pytest.raises(AdaspaError):
+        SearchSchedule(bad)

@@ -1,0 +1,101 @@
+"""The two-phase search schedule on the GPU (overview figure; Sec. 4.2;
+Algorithms 1 and 2) on a small drifted workload, X_t = X_0 + (0.05 t / 8) E
+with one fixed draw E per tensor, search steps T_s = {2, 5}, TOPK keep 25%.
+
+The oracle derives both block patterns itself from the seeded inputs: the
+fused search at t = 2 from the masses of X_2 with X_2's own LSE, the
+LSE-cached search at t = 5 from the masses of X_5 with the LSE kept at t = 2.
+The GPU's masses must match the oracle's, its lists must be valid top-k
+selections of them (identical up to near ties), and every step's output must
+match the oracle's: dense before and at t = 2, masked attention with the
+oracle's pattern afterwards (on the rows whose GPU list is the oracle's)."""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from paper_2502_21079_amd.schedule import (CACHED_SEARCH, DENSE, FUSED_SEARCH, SPARSE,
+                                           AdaSpaAttention, SearchSchedule)
+from workloads import TINY, make_drift_noise, make_qkv, text_blocks
+from _helpers import check_lse, check_mass, check_out, csr_rows, f64
+
+pytestmark = pytest.mark.gpu
+
+STEPS, KEEP = 8, 2500
+
+
+def _oracle_pattern(W, w):
+    return oracle.select_blocks(W[None].astype(np.float32), w.seqlen, w.block, w.text_start,
+                                w.text_len, "topk", [KEEP] * w.heads)
+
+
+def _check_lists(res, sel, W, w):
+    """GPU lists valid against the oracle's masses; returns the rows equal to
+    the oracle's lists."""
+    rp, ci = csr_rows(res.row_ptr, res.col_idx)
+    nb = w.nblocks
+    tk = set(text_blocks(w.seqlen, w.block, w.text_start, w.text_len))
+    same = set()
+    for h in range(w.heads):
+        kh = int(sel["head_k"][0, h])
+        assert int(res.head_k[0, h]) == kh
+        for p in range(nb):
+            r = h * nb + p
+            got = ci[rp[r]:rp[r + 1]]
+            exp = sel["col_idx"][sel["row_ptr"][r]:sel["row_ptr"][r + 1]]
+            if np.array_equal(got, exp):
+                same.add(r)
+                continue
+            assert len(got) == len(exp) and tk <= set(got.tolist()), (h, p)
+            others = np.sort(np.array([W[h, p, c] for c in range(nb) if c not in tk]))[::-1]
+            kth = others[kh - len(tk) - 1]
+            for c in set(got.tolist()) ^ set(exp.tolist()):
+                assert abs(W[h, p, c] - kth) <= 1e-3 * kth, (h, p, c)
+    return same
+
+
+def test_two_phase_schedule_against_oracle():
+    w = TINY
+    x0 = make_qkv(w, device="cuda", fp32=True)
+    eps = make_drift_noise(w, device="cuda", seed=4)
+    layer = AdaSpaAttention((w.batch, w.heads, w.seqlen, w.head_dim), block=w.block,
+                            text_start=w.text_start, text_len=w.text_len, mode="topk",
+                            head_param_bp=[KEEP] * w.heads, schedule=SearchSchedule((2, 5)))
+    nb = w.nblocks
+    lse2 = None            # the oracle's LSE of the fused-search step (per head)
+    pattern = None         # the oracle's current pattern
+    same_rows = set()
+    for t in range(STEPS):
+        q, k, v = [(x0[i] + (0.05 * t / STEPS) * eps[i]).to(torch.bfloat16) for i in range(3)]
+        out, act = layer.step(t, q, k, v)
+        torch.cuda.synchronize()
+        heads = [(f64(q[0, h]), f64(k[0, h]), f64(v[0, h])) for h in range(w.heads)]
+        if act in (DENSE, FUSED_SEARCH):
+            assert act == (DENSE if t < 2 else FUSED_SEARCH), t
+            for h, (qh, kh, vh) in enumerate(heads):
+                o_ref, l_ref = oracle.dense_attention(qh, kh, vh, w.scale)
+                check_out(out[0, h], o_ref, f"t{t} h{h}")
+                if act == FUSED_SEARCH:
+                    check_lse(layer.lse[0, h], l_ref, f"t{t} lse h{h}")
+        if act in (FUSED_SEARCH, CACHED_SEARCH):
+            if act == FUSED_SEARCH:
+                lse2 = [oracle.dense_attention(qh, kh, vh, w.scale)[1] for qh, kh, vh in heads]
+            # fused search: the fresh LSE of this step; cached search: the LSE kept at t = 2
+            W = np.stack([oracle.block_mass(qh, kh, lse2[h], w.scale, w.block)
+                          for h, (qh, kh, _) in enumerate(heads)])
+            for h in range(w.heads):
+                check_mass(layer.search.block_mass[0, h], W[h], f"t{t} mass h{h}")
+            pattern = _oracle_pattern(W, w)
+            same_rows = _check_lists(layer.search, pattern, W, w)
+            assert layer.search_step == t and layer.lse_step == 2
+            assert len(same_rows) >= 0.9 * w.heads * nb
+        if act in (SPARSE, CACHED_SEARCH):
+            assert act == (CACHED_SEARCH if t == 5 else SPARSE), t
+            for h, (qh, kh, vh) in enumerate(heads):
+                o_ref, l_ref = oracle.block_sparse_attention(
+                    qh, kh, vh, pattern["row_ptr"][h * nb:(h + 1) * nb + 1], pattern["col_idx"],
+                    w.scale, w.block)
+                for p in range(nb):
+                    if h * nb + p in same_rows:
+                        rows = slice(p * w.block, (p + 1) * w.block)
+                        check_out(out[0, h, rows], o_ref[rows], f"t{t} h{h} p{p}")
