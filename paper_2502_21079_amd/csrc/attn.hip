@@ -442,9 +442,9 @@ __global__ __launch_bounds__(64 * NW, NW >= 8 ? 1 : 2) void attn_sparse_pair_ker
   constexpr int KS = KDMA::S, VS = VDMA::S;
   constexpr int ND = D / 32;
   constexpr int NK = D / 16;
-  static_assert(VDMA::ELEMS * 2 >= kMaxBlocks, "the V slot holds the block map");
   using LD = KVLoader<D, NW>;
   __shared__ __attribute__((aligned(1024))) u16 sKV[2][LD::ELEMS];   // slots [K | V]
+  __shared__ uint8_t sMap[kMaxBlocks];                                 // the rows' block map
   const SlotPart<LD::ELEMS, 0> sK{sKV};
   const SlotPart<LD::ELEMS, LD::VOFF> sV{sKV};
 
@@ -476,7 +476,7 @@ __global__ __launch_bounds__(64 * NW, NW >= 8 ? 1 : 2) void attn_sparse_pair_ker
   const int klane = (c32 * KS + hw) * 8;
 
 #pragma unroll
-  for (int b = 0; b < 2; ++b) zero_lds<VDMA::SLOTS>(sV[b], tid, NT);   // finite V; the block map
+  for (int b = 0; b < 2; ++b) zero_lds<VDMA::SLOTS>(sV[b], tid, NT);   // finite V
   bf16x8 qf[NK];
   load_q<D>(a.q + hoff, qrow, L, hw, qf);
   // As in attn_fwd_kernel: under the text sink the union of the two rows
@@ -538,58 +538,74 @@ __global__ __launch_bounds__(64 * NW, NW >= 8 ? 1 : 2) void attn_sparse_pair_ker
       last = __builtin_amdgcn_readlane(v, 63);
     }
   }
-  // Size of the union: |A| + |B| - |A and B|, the intersection counted with a
-  // byte map of row A's blocks in V slot 0 (read before that slot's first
-  // load, which follows the prologue's barriers).
-  uint8_t* mark = reinterpret_cast<uint8_t*>(sV[0]);
-  int inter = 0;
-  __syncthreads();                    // slot 0 zeroed by every thread
+  // Byte map of the two rows' key blocks (bit 0: block 2P keeps it, bit 1:
+  // block 2P+1 keeps it), without the ragged block (done masked at the end).
+  // Shared blocks run as full steps for all 128 rows (phase 1); the blocks
+  // only one row keeps run afterwards as dual half steps (phase 2): each
+  // step holds 32 keys of one solo block of each row, so neither half
+  // computes for a tile it does not keep.
+  static_assert(SUB == 1, "one 64-key tile per block");
+  int n_shared = 0;
   if (!slow) {
+    for (int i = tid; i < nkb; i += NT) sMap[i] = 0;
+    __syncthreads();
     for (int c = 0; c * 64 < len[0]; ++c) {
       const int v = chunk(0, c);
-      if (c * 64 + lane < len[0]) mark[v] = 1;
+      if (c * 64 + lane < len[0] && !(ragged_L && v == nkb - 1)) sMap[v] = 1;
     }
-  }
-  __syncthreads();
-  if (!slow) {
+    __syncthreads();
+    // Every wave writes the same value (bit 0 is final after the barrier
+    // and kept), so the waves' writes agree whatever their order, and every
+    // wave counts the same shared blocks from bit 0.
     for (int c = 0; c * 64 < len[1]; ++c) {
       const int v = chunk(1, c);
-      inter += __builtin_popcountll(__ballot(c * 64 + lane < len[1] && mark[v] == 1));
+      const bool in = c * 64 + lane < len[1] && !(ragged_L && v == nkb - 1);
+      const int a_keeps = in ? (sMap[v] & 1) : 0;
+      if (in) sMap[v] = (uint8_t)(a_keeps | 2);
+      n_shared += __builtin_popcountll(__ballot(a_keeps != 0));
     }
   }
-  // The pipeline walks the union without the ragged block (done masked);
-  // pipeline tile j is 64-key tile j % SUB of union entry j / SUB.
+  // Dual half steps pay off when both rows have solo blocks in similar
+  // numbers (a half step costs a little over half a full step).  Otherwise
+  // (one row has none, as for the single block of the last pair when NB is
+  // odd, or a text row beside a video row) phase 1 walks the whole union in
+  // ascending order instead, the half that does not keep a tile taking it
+  // hidden, and there is no phase 2.
   const int na = len[0] - (rag & 1), nb = len[1] - ((rag >> 1) & 1);
-  const int nu = slow ? 0 : na + nb - (inter - (rag == 3 ? 1 : 0));
-  const int nf = nu * SUB;
+  const int nAs = na - n_shared, nBs = nb - n_shared;
+  const int s_min = nAs < nBs ? nAs : nBs, s_max = nAs < nBs ? nBs : nAs;
+  const bool dual = !slow && s_min > 0 && s_min * 6 > s_max;
+  const int nf1 = slow ? 0 : (dual ? n_shared : na + nb - n_shared);   // phase 1: full steps
+  const int cls1 = dual ? 3 : 0;                           // its blocks: shared, or the union
+  const int nA2 = dual ? 2 * nAs : 0;                      // phase 2: half tiles of each row
+  const int nB2 = dual ? 2 * nBs : 0;
+  const int nf2 = nA2 > nB2 ? nA2 : nB2;
+  const int half = wave / WPB;                             // 0: block 2P, 1: block 2P+1
+  const int n_mine = half == 0 ? nA2 : nB2;
 
-  // Merge state: next unread entry of each row (windows w0/w1 above).
-  int head[2] = {0, 0}, win[2] = {0, 0};
-  // Next block of the union (ascending) and which rows keep it; both heads
-  // are read before a window moves (the new chunk is first read 64 entries
-  // later).
-  auto next_union = [&](int& blk, int& keep) {
-    int v[2];
-#pragma unroll
-    for (int r = 0; r < 2; ++r) {
-      const int i = head[r];
-      const int x0 = __builtin_amdgcn_readlane(w0[r], i & 63);
-      const int x1 = __builtin_amdgcn_readlane(w1[r], i & 63);
-      v[r] = i < (r == 0 ? na : nb) ? ((i >> 6) == win[r] ? x0 : x1) : INT_MAX;
+  // Blocks of one class of the map in ascending order (cls 3: both rows keep
+  // it, 1 or 2: only that row, 0: either), 64 map entries at a time (ballots
+  // over the window, then the set bits); -1 when exhausted.  keep receives
+  // the block's map entry.
+  struct MapStream {
+    int w;
+    uint64_t m, ma, mb;
+  };
+  const int nwin = (nkb + 63) / 64;
+  auto next_of = [&](MapStream& st, int cls, int& keep) -> int {
+    while (st.m == 0ull) {
+      if (++st.w >= nwin) return -1;
+      const int blk = st.w * 64 + lane;
+      const int v = blk < nkb ? sMap[blk] : 0;
+      st.ma = __ballot((v & 1) != 0);
+      st.mb = __ballot((v & 2) != 0);
+      st.m = cls == 0 ? (st.ma | st.mb)
+                      : (cls == 3 ? (st.ma & st.mb) : (cls == 1 ? (st.ma & ~st.mb) : (st.mb & ~st.ma)));
     }
-    blk = v[0] < v[1] ? v[0] : v[1];
-    keep = (v[0] == blk ? 1 : 0) | (v[1] == blk ? 2 : 0);
-#pragma unroll
-    for (int r = 0; r < 2; ++r) {
-      if (keep & (1 << r)) {
-        ++head[r];
-        if ((head[r] >> 6) > win[r]) {
-          w0[r] = w1[r];
-          w1[r] = load_chunk(r, win[r] + 2);
-          ++win[r];
-        }
-      }
-    }
+    const int j = __builtin_ctzll(st.m);
+    st.m &= st.m - 1;
+    keep = (int)((st.ma >> j) & 1ull) | ((int)((st.mb >> j) & 1ull) << 1);
+    return st.w * 64 + j;
   };
 
   const float sl2 = a.scale_log2;
@@ -607,23 +623,42 @@ __global__ __launch_bounds__(64 * NW, NW >= 8 ? 1 : 2) void attn_sparse_pair_ker
   __shared__ int s_redo;              // as in attn_fwd_kernel
   if (tid == 0) s_redo = 0;
   bool redo = false;
-  __syncthreads();                    // block map reads done
+  __syncthreads();                    // the map is complete
 
-  if (nf > 0) {
-    // Union entries u0 = t / SUB, u0 + 1, u0 + 2 (block, keep bits) at step t.
-    int ub[3] = {0, 0, 0}, uk[3] = {0, 0, 0};
-    int u0 = 0;
+  bf16x8 p_prev[2][2];
+  bool pend = false;
+  float pend_alpha = 1.f;
+  RowSums rsum;
+  rsum.init(lane);
+  bool bad = false;
+  LD ld;
+  ld.init(wave, lane);
+  const u32x4 rMw = ld.mixed_v ? rVw : rKw;     // resource of this wave's mixed entry
+  auto rescale_pending = [&]() {
+    if (pend) {             // the reference moved at the previous step
 #pragma unroll
-    for (int j = 0; j < 3; ++j)
-      if (j < nu) next_union(ub[j], uk[j]);
-    auto pick = [&](const int (&x)[3], int slot) { return slot == 0 ? x[0] : (slot == 1 ? x[1] : x[2]); };
-    // First row of pipeline tile j, j within the queue's reach.
-    auto tile_row = [&](int j) { return (pick(ub, j / SUB - u0) * SUB + j % SUB) * KT; };
-    const int r0 = tile_row(0), r1 = nf > 1 ? tile_row(1) : -1;
-    if (!(g0 >= 0 && r0 == g0 && (nf < 2 || r1 == g1))) {
+      for (int d = 0; d < ND; ++d)
+#pragma unroll
+        for (int e = 0; e < 16; ++e) o[d][e] *= pend_alpha;
+      pend = false;
+    }
+  };
+
+  if (nf1 > 0) {
+    // Phase 1: blocks u0 = t, t + 1, t + 2 at step t (block, map entry), as
+    // in attn_fwd_kernel.
+    MapStream ss{-1, 0ull, 0ull, 0ull};
+    int ub[3], uk[3] = {0, 0, 0};
+#pragma unroll
+    for (int j = 0; j < 3; ++j) ub[j] = next_of(ss, cls1, uk[j]);
+    int u0 = 0;
+    auto pick = [&](int slot) { return slot == 0 ? ub[0] : (slot == 1 ? ub[1] : ub[2]); };
+    auto tile_row = [&](int j) { return pick(j - u0) * BLK; };    // j within the queue's reach
+    const int r0 = tile_row(0), r1 = nf1 > 1 ? tile_row(1) : -1;
+    if (!(g0 >= 0 && r0 == g0 && (nf1 < 2 || r1 == g1))) {
       if (g0 >= 0) wait_vmem();          // this wave's guessed loads land first
       KDMA::issue(rK, sK[0], r0, wave, lane);
-      if (nf > 1) KDMA::issue(rK, sK[1], r1, wave, lane);
+      if (nf1 > 1) KDMA::issue(rK, sK[1], r1, wave, lane);
     }
     wait_vmem();
     __syncthreads();
@@ -631,40 +666,17 @@ __global__ __launch_bounds__(64 * NW, NW >= 8 ? 1 : 2) void attn_sparse_pair_ker
     qk_tile<D, KS>(sK[0], qf, c32, hw, s_cur);
     bool hid = !(uk[0] & mybit);
     __syncthreads();                  // sK[0] is refilled by step 0
-
-    bf16x8 p_prev[2][2];
 #pragma unroll
     for (int g = 0; g < 2; ++g)
 #pragma unroll
       for (int s2 = 0; s2 < 2; ++s2) p_prev[g][s2] = bf16x8{};
-    bool pend = false;
-    float pend_alpha = 1.f;
-    RowSums rsum;
-    rsum.init(lane);
-    bool bad = false;
-    LD ld;
-    ld.init(wave, lane);
-    const u32x4 rMw = ld.mixed_v ? rVw : rKw;     // resource of this wave's mixed entry
 
-    // Step t reads K(t+1) and V(t-1) from slot RS and loads K(t+2) and V(t)
-    // into the other slot, as in attn_fwd_kernel (the K index clamped to the
-    // last tile past the end); tile j is union entry j.
     auto step = [&](int t, auto rs_c) {
       constexpr int RS = decltype(rs_c)::value;
-      const u16* rdK = sK[RS];
-      const u16* rdV = sV[RS];
-      if (pend) {             // the reference moved at the previous step
-#pragma unroll
-        for (int d = 0; d < ND; ++d)
-#pragma unroll
-          for (int e = 0; e < 16; ++e) o[d][e] *= pend_alpha;
-        pend = false;
-      }
-      uint32_t kbyte = (uint32_t)tile_row(t + 2 < nf ? t + 2 : nf - 1) * (uint32_t)(D * 2);
+      rescale_pending();
+      uint32_t kbyte = (uint32_t)tile_row(t + 2 < nf1 ? t + 2 : nf1 - 1) * (uint32_t)(D * 2);
       uint32_t vbyte = (uint32_t)tile_row(t) * (uint32_t)(D * 2);
       asm volatile("" : "+s"(kbyte), "+s"(vbyte));
-      u16* ldK = sK[1 - RS];
-      u16* ldV = sV[1 - RS];
       uint32_t fill = lds_addr(sKV[1 - RS]);
       asm volatile("" : "+s"(fill));
       const uint32_t mbyte = ld.mixed_v ? vbyte : kbyte;
@@ -677,8 +689,8 @@ __global__ __launch_bounds__(64 * NW, NW >= 8 ? 1 : 2) void attn_sparse_pair_ker
       };
       f32x16 s_next[2];
       bf16x8 p_cur[2][2];
-      pipelined_step<D, KS, VS>(loads, rdK + klane, rdV + voff, qf, s_cur, p_prev, s_next, p_cur, o, sl2,
-                                hid ? INFINITY : ref.mc, rsum);
+      pipelined_step<D, KS, VS>(loads, sK[RS] + klane, sV[RS] + voff, qf, s_cur, p_prev, s_next, p_cur, o,
+                                sl2, hid ? INFINITY : ref.mc, rsum);
       move_reference(ref, rsum, bad, s_cur, p_cur, pend, pend_alpha, sl2, c32, hid);
 #pragma unroll
       for (int g = 0; g < 2; ++g) {
@@ -686,32 +698,107 @@ __global__ __launch_bounds__(64 * NW, NW >= 8 ? 1 : 2) void attn_sparse_pair_ker
 #pragma unroll
         for (int s2 = 0; s2 < 2; ++s2) p_prev[g][s2] = p_cur[g][s2];
       }
-      hid = !(pick(uk, (t + 1) / SUB - u0) & mybit);   // tile t+1
-      if ((t + 1) % SUB == 0) {          // tile t was the last of entry u0
-        ub[0] = ub[1];
-        uk[0] = uk[1];
-        ub[1] = ub[2];
-        uk[1] = uk[2];
-        if (u0 + 3 < nu) next_union(ub[2], uk[2]);
-        ++u0;
+      hid = !(uk[1] & mybit);          // tile t+1
+      ub[0] = ub[1];
+      uk[0] = uk[1];
+      ub[1] = ub[2];
+      uk[1] = uk[2];
+      if (u0 + 3 < nf1) ub[2] = next_of(ss, cls1, uk[2]);
+      ++u0;
+      wait_vmem();
+      __syncthreads();
+    };
+    int t = 0;
+    for (; t + 1 < nf1; t += 2) {
+      step(t, std::integral_constant<int, 1>{});
+      step(t + 1, std::integral_constant<int, 0>{});
+    }
+    if (t < nf1) step(t, std::integral_constant<int, 1>{});
+    rescale_pending();
+    pv_tile<ND, VS>(sV[(nf1 - 1) & 1] + voff, p_prev, o);
+#pragma unroll
+    for (int j = 0; j < 4; ++j) rsum.add(p_prev[j >> 1][j & 1]);
+    bad = bad || !(rsum.acc[0] <= kRowSumBad);
+  }
+
+  if (nf2 > 0) {
+    // Phase 2: dual half steps.  Half tile t of a row is keys [32 (t % 2),
+    // 32 (t % 2) + 32) of its (t / 2)-th solo block; rows [0, 32) of a slot
+    // hold block 2P's half tile, rows [32, 64) block 2P+1's, and each half of
+    // the workgroup reads its own rows.  A row with fewer half tiles than the
+    // other takes its surplus steps hidden (key 0 loaded in their place).
+    if (nf1 == 0 && g0 >= 0) wait_vmem();   // the guessed loads land before these
+    MapStream sa{-1, 0ull, 0ull, 0ull}, sb{-1, 0ull, 0ull, 0ull};
+    int qa[2], qb[2], kp;                    // solo blocks of half tiles t and t + 2
+    qa[0] = next_of(sa, 1, kp);
+    qa[1] = next_of(sa, 1, kp);
+    qb[0] = next_of(sb, 2, kp);
+    qb[1] = next_of(sb, 2, kp);
+    auto key = [](int t, int n, int blk) { return t < n ? blk * BLK + 32 * (t & 1) : 0; };
+    TileDMA<D, NW, 1>::issue_dual(rK, sK[0], key(0, nA2, qa[0]), key(0, nB2, qb[0]), wave, lane);
+    TileDMA<D, NW, 1>::issue_dual(rK, sK[1], key(1, nA2, qa[0]), key(1, nB2, qb[0]), wave, lane);
+    wait_vmem();
+    __syncthreads();
+    const int klane_h = klane + half * 32 * KS * 8;
+    const int voff_h = voff + half * 32 * VS * 8;
+    const uint32_t hmask = LD::half_mask(wave, lane);
+    f32x16 s_cur[2];
+    qk_tile<D, KS, 1>(sK[0] + klane_h - klane, qf, c32, hw, s_cur);
+    bool hid = 0 >= n_mine;
+    __syncthreads();                  // sK[0] is refilled by step 0
+#pragma unroll
+    for (int s2 = 0; s2 < 2; ++s2) p_prev[0][s2] = bf16x8{};
+
+    auto step2 = [&](int t, auto rs_c) {
+      constexpr int RS = decltype(rs_c)::value;
+      rescale_pending();
+      constexpr uint32_t HALF_BYTES = 32u * D * 2u;
+      uint32_t ka = (uint32_t)key(t + 2, nA2, qa[1]) * (uint32_t)(D * 2);
+      uint32_t kb = (uint32_t)key(t + 2, nB2, qb[1]) * (uint32_t)(D * 2) - HALF_BYTES;
+      uint32_t va = (uint32_t)key(t, nA2, qa[0]) * (uint32_t)(D * 2);
+      uint32_t vb = (uint32_t)key(t, nB2, qb[0]) * (uint32_t)(D * 2) - HALF_BYTES;
+      asm volatile("" : "+s"(ka), "+s"(kb), "+s"(va), "+s"(vb));
+      uint32_t fill = lds_addr(sKV[1 - RS]);
+      asm volatile("" : "+s"(fill));
+      auto loads = [&](int slot) {      // loads in the first PW slots of the step
+        constexpr int PW = LD::PW;
+        if (slot >= PW) return;
+        ld.issue_dual_n(slot, fill, rKw, rVw, rMw, ka, kb, va, vb, hmask);
+      };
+      f32x16 s_next[2];
+      bf16x8 p_cur[2][2];
+      pipelined_step<D, KS, VS, 1>(loads, sK[RS] + klane_h, sV[RS] + voff_h, qf, s_cur, p_prev, s_next,
+                                   p_cur, o, sl2, hid ? INFINITY : ref.mc, rsum);
+      move_reference<1>(ref, rsum, bad, s_cur, p_cur, pend, pend_alpha, sl2, c32, hid);
+      s_cur[0] = s_next[0];
+#pragma unroll
+      for (int s2 = 0; s2 < 2; ++s2) p_prev[0][s2] = p_cur[0][s2];
+      hid = t + 1 >= n_mine;
+      if (t & 1) {                        // half tile t was the second of its block
+        qa[0] = qa[1];
+        qa[1] = next_of(sa, 1, kp);
+        qb[0] = qb[1];
+        qb[1] = next_of(sb, 2, kp);
       }
       wait_vmem();
       __syncthreads();
     };
     int t = 0;
-    for (; t + 1 < nf; t += 2) {
-      step(t, std::integral_constant<int, 1>{});
-      step(t + 1, std::integral_constant<int, 0>{});
+    for (; t + 1 < nf2; t += 2) {
+      step2(t, std::integral_constant<int, 1>{});
+      step2(t + 1, std::integral_constant<int, 0>{});
     }
-    if (t < nf) step(t, std::integral_constant<int, 1>{});
-    if (pend) {
+    if (t < nf2) step2(t, std::integral_constant<int, 1>{});
+    rescale_pending();
+    pv_tile<ND, VS, 1>(sV[(nf2 - 1) & 1] + voff_h, p_prev, o);
 #pragma unroll
-      for (int d = 0; d < ND; ++d)
-#pragma unroll
-        for (int e = 0; e < 16; ++e) o[d][e] *= pend_alpha;
-    }
-    pv_tile<ND, VS>(sV[(nf - 1) & 1] + voff, p_prev, o);
-    lsum = finish_sums(rsum, bad, p_prev, hw, c32);
+    for (int s2 = 0; s2 < 2; ++s2) rsum.add(p_prev[0][s2]);
+    bad = bad || !(rsum.acc[0] <= kRowSumBad);
+  }
+
+  if (nf1 + nf2 > 0) {
+    const float v = RowSums::for_row(rsum.acc[0], c32);
+    lsum = hw == 0 ? v : 0.f;
     bad = bad || !acc_finite<ND>(o);
     redo = __any(bad);
     if (redo && lane == 0) s_redo = 1;
@@ -763,7 +850,7 @@ __global__ __launch_bounds__(64 * NW, NW >= 8 ? 1 : 2) void attn_sparse_pair_ker
     for (int j = 0; j < SUB; ++j)
       if ((nkb - 1) * BLK + j * KT < L) masked_tile((nkb - 1) * BLK + j * KT, rag, !redo);
   }
-  if (nf == 0 && g0 >= 0) wait_vmem();      // no guessed load is left in flight
+  if (nf1 + nf2 == 0 && g0 >= 0) wait_vmem();   // no guessed load is left in flight
 
   float lt;
   {

@@ -102,6 +102,24 @@ struct TileDMA {
     }
   }
 
+  // Issue the loads of a dual tile: rows [0, 32) from keys [ka, ka + 32),
+  // rows [32, 64) from keys [kb, kb + 32) (both inside the sequence).  Pad
+  // slots use an out-of-range offset: the load is skipped.
+  __device__ __forceinline__ static void issue_dual(__amdgpu_buffer_rsrc_t r, u16* dst, int ka, int kb,
+                                                    int wave, int lane) {
+#pragma unroll
+    for (int i0 = 0; i0 < NINST; i0 += NW) {
+      const int i = i0 + wave;
+      if (i < NINST) {
+        const int p = i * 64 + lane;
+        const int row = p / S, ch = p % S;
+        const int key = row < 32 ? ka + row : kb + (row - 32);
+        const uint32_t off = ch < CPR ? (uint32_t)(key * D + ch * 8) * 2u : 0xFFFFFFF0u;
+        __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (lds_void*)(dst + i * 64 * 8), 16, off, 0, 0, 0);
+      }
+    }
+  }
+
   // Byte offset, inside the tile, of the chunk that slot i * 64 + lane loads
   // when every row of the tile lies inside the sequence.  A pad slot loads a
   // copy of its row's last data chunk (it is never read, and an in-range
@@ -222,6 +240,45 @@ struct KVLoader {
       else issue_n<J + 1>(n, slot, rK, rV, rM, kbyte, vbyte, mbyte);
     }
   }
+
+  // Dual slots: rows [0, 32) of the K and V tiles come from one 32-key half
+  // tile, rows [32, 64) from another.  Bit j of the returned mask is set when
+  // this lane's load j fills a row of the second half (the pieces and their
+  // assignment to the waves are those above).
+  __device__ __forceinline__ static uint32_t half_mask(int wave, int lane) {
+    uint32_t m = 0;
+#pragma unroll
+    for (int j = 0; j < PW; ++j) {
+      int f = j * NW + wave;
+      if (f >= NTOT) f -= NW;
+      const int row = f < NK ? (f * 64 + lane) / K::S : ((f - NK) * 64 + lane) / V::S;
+      if (row >= 32) m |= 1u << j;
+    }
+    return m;
+  }
+  // Load J of a dual slot: ka / va are the first bytes of the first half's
+  // K / V keys, kb / vb those of the second half's minus 32 rows (the in-tile
+  // offsets of its rows start at row 32), and the lane adds the one of the
+  // half its row belongs to; the scalar offset is zero.
+  template <int J>
+  __device__ __forceinline__ void issue_dual(uint32_t slot, u32x4 rK, u32x4 rV, u32x4 rM, uint32_t ka,
+                                             uint32_t kb, uint32_t va, uint32_t vb, uint32_t hmask) const {
+    constexpr int F = J * NW * 1024;
+    const bool second = (hmask >> J) & 1u;
+    const uint32_t kk = second ? kb : ka, vv = second ? vb : va;
+    if constexpr (J == PW - 1) dma16<F>(rV, slot + wlast, rel[J] + vv, 0u);
+    else if constexpr (all_k(J)) dma16<F>(rK, slot + wbase, rel[J] + kk, 0u);
+    else if constexpr (all_v(J)) dma16<F>(rV, slot + wbase, rel[J] + vv, 0u);
+    else dma16<F>(rM, slot + wbase, rel[J] + (mixed_v ? vv : kk), 0u);
+  }
+  template <int J = 0>
+  __device__ __forceinline__ void issue_dual_n(int n, uint32_t slot, u32x4 rK, u32x4 rV, u32x4 rM, uint32_t ka,
+                                               uint32_t kb, uint32_t va, uint32_t vb, uint32_t hmask) const {
+    if constexpr (J < PW) {
+      if (n == J) issue_dual<J>(slot, rK, rV, rM, ka, kb, va, vb, hmask);
+      else issue_dual_n<J + 1>(n, slot, rK, rV, rM, ka, kb, va, vb, hmask);
+    }
+  }
 };
 
 // The K or V part of the ring slots: part[b] is the tile in slot b.
@@ -255,14 +312,15 @@ __device__ __forceinline__ void load_q(const u16* qh, int qrow, int L, int hw, b
   }
 }
 
-// S^T tile for two groups of 32 keys: lane (hw, c32) gets keys
-// 32g + 8(e/4) + 4hw + e%4 of query c32 in s[g][e].
-template <int D, int S>
+// S^T tile for G groups of 32 keys (G = 2: a 64-key tile; G = 1: its first
+// 32 keys): lane (hw, c32) gets keys 32g + 8(e/4) + 4hw + e%4 of query c32 in
+// s[g][e].
+template <int D, int S, int G = 2>
 __device__ __forceinline__ void qk_tile(const u16* sK, const bf16x8 (&qf)[D / 16], int c32, int hw,
                                         f32x16 (&s)[2]) {
   const u16* base = sK + (c32 * S + hw) * 8;
 #pragma unroll
-  for (int g = 0; g < 2; ++g) {
+  for (int g = 0; g < G; ++g) {
     s[g] = f32x16{};
 #pragma unroll
     for (int ks = 0; ks < D / 16; ++ks) {
@@ -310,10 +368,11 @@ struct RowRef {
   // m <- max(m, row maximum of s) for the rows of this wave (the two
   // half-waves holding a row agree); returns the rescale factor of sums
   // taken against the old reference.
+  template <int G = 2>
   __device__ __forceinline__ float raise(const f32x16 (&s)[2], float sl2) {
     float mt = -INFINITY;
 #pragma unroll
-    for (int g = 0; g < 2; ++g)
+    for (int g = 0; g < G; ++g)
 #pragma unroll
       for (int e = 0; e < 16; e += 2) mt = vmax(mt, vmax(s[g][e], s[g][e + 1]));
     float lo, hi;
@@ -370,11 +429,12 @@ struct RowSums {
 // P = bf16(exp2(s * sl2 - mc)) for one S^T tile; returns this lane's sum of
 // exactly the rounded values that enter P V, so numerator and denominator
 // use the same weights.
+template <int G = 2>
 __device__ __forceinline__ float exp_tile(const f32x16 (&s)[2], float sl2, float mc, bf16x8 (&pb)[2][2]) {
   const bf16x2 ones = {(__bf16)1.0f, (__bf16)1.0f};
   float ts = 0.f;
 #pragma unroll
-  for (int g = 0; g < 2; ++g)
+  for (int g = 0; g < G; ++g)
 #pragma unroll
     for (int e = 0; e < 16; e += 2) {
       const bf16x2 pr = {(__bf16)fast_exp2(fmaf(s[g][e], sl2, -mc)),
@@ -395,6 +455,7 @@ __device__ __forceinline__ float exp_tile(const f32x16 (&s)[2], float sl2, float
 // new reference.  bad is set when a sum has left the safe range.  A hidden
 // tile (block-64 pairs: one the other query block keeps) never sets the
 // reference and its probabilities stay exact zeros.
+template <int G = 2>
 __device__ __forceinline__ void move_reference(RowRef& ref, RowSums& rsum, bool& bad,
                                                const f32x16 (&s_cur)[2], bf16x8 (&p_cur)[2][2],
                                                bool& pend, float& pend_alpha, float sl2, int c32,
@@ -409,24 +470,25 @@ __device__ __forceinline__ void move_reference(RowRef& ref, RowSums& rsum, bool&
   const float d = RowSums::for_row(dr, c32);        // the same value for this lane's row
   float al;
   if (ref.m == -INFINITY) {
-    al = hidden ? 1.f : ref.raise(s_cur, sl2);
+    al = hidden ? 1.f : ref.template raise<G>(s_cur, sl2);
   } else {
     if (d > 0.f) ref.shift(d, sl2);
     al = fast_exp2(-d);
   }
   pend_alpha = al;
   pend = true;
-  exp_tile(s_cur, sl2, hidden ? INFINITY : ref.mc, p_cur);
+  exp_tile<G>(s_cur, sl2, hidden ? INFINITY : ref.mc, p_cur);
 }
 
 // After the last pipelined tile: its probabilities join the sums, a sum out
 // of the safe range sets bad, and the row's sum is returned in the form the
 // masked path continues from (the whole sum on the hw = 0 lane of the row, 0
 // on the other).
+template <int G = 2>
 __device__ __forceinline__ float finish_sums(RowSums& rsum, bool& bad, const bf16x8 (&p_last)[2][2],
                                              int hw, int c32) {
 #pragma unroll
-  for (int j = 0; j < 4; ++j) rsum.add(p_last[j >> 1][j & 1]);
+  for (int j = 0; j < 2 * G; ++j) rsum.add(p_last[j >> 1][j & 1]);
   const float sr = rsum.acc[0];
   bad = bad || !(sr <= kRowSumBad);
   const float v = RowSums::for_row(sr, c32);
@@ -470,12 +532,12 @@ __device__ __forceinline__ float softmax_tile(const f32x16 (&s)[2], RowRef& ref,
 // 32g + 16s2 + 8u + 4hw + j; lane (hw, e) supplies key index 8*(e/4) + 4*hw +
 // e%4 of the step.  In each 16-lane group, lane j names row r0 + j/4 and 4
 // elements at column d*32 + 16*(grp&1) + 4*(j%4); vlane is that lane's base.
-template <int ND, int VS>
+template <int ND, int VS, int G = 2>
 __device__ __forceinline__ void pv_tile(const u16* vlane, const bf16x8 (&pb)[2][2], f32x16 (&o)[ND]) {
 #pragma unroll
   for (int d = 0; d < ND; ++d)
 #pragma unroll
-    for (int g = 0; g < 2; ++g)
+    for (int g = 0; g < G; ++g)
 #pragma unroll
       for (int s2 = 0; s2 < 2; ++s2) {
         const u16* p0 = vlane + (32 * g + 16 * s2) * VS * 8 + d * 32;
@@ -501,24 +563,25 @@ __device__ __forceinline__ void pv_tile(const u16* vlane, const bf16x8 (&pb)[2][
 // pipe and the VALU work side by side within the wave.  Four slots also add
 // the previous tile's rounded probabilities (the operands of its P V) to the
 // running row sums.
-template <int D, int KS, int VS, typename Hook>
+template <int D, int KS, int VS, int G = 2, typename Hook>
 __device__ __forceinline__ void pipelined_step(Hook&& hook, const u16* klane, const u16* vlane,
                                                const bf16x8 (&qf)[D / 16], const f32x16 (&s_cur)[2],
                                                const bf16x8 (&p_prev)[2][2], f32x16 (&s_next)[2],
                                                bf16x8 (&p_cur)[2][2], f32x16 (&o)[D / 32], float sl2,
                                                float mc, RowSums& rsum) {
   constexpr int NK = D / 16, ND = D / 32;
-  constexpr int NQK = 2 * NK, NPV = 4 * ND;
+  constexpr int NQK = G * NK, NPV = 2 * G * ND;      // G score groups of 32 keys
   static_assert(NQK == NPV, "QK and PV slots alternate");
   constexpr int NM = NQK + NPV;
-  static_assert(32 % NM == 0 && NM % 2 == 0, "whole exponential pairs per slot pair");
+  constexpr int NS = 16 * G;                           // scores per lane
+  static_assert(NS % NM == 0 && NM % 2 == 0, "whole exponential pairs per slot pair");
   constexpr int LA = 2;                       // operand lookahead, in slots
 
   bf16x8 op[NM];
   auto fetch = [&](int i) {
     const int j = i >> 1;
-    if ((i & 1) == 0) {       // QK j: g = j % 2, ks = j / 2
-      const int g = j & 1, ks = j >> 1;
+    if ((i & 1) == 0) {       // QK j: g = j % G, ks = j / G
+      const int g = j % G, ks = j / G;
       op[i] = *reinterpret_cast<const bf16x8*>(klane + (32 * g * KS + 2 * ks) * 8);
     } else {                  // PV j: d = j % ND, (g, s2) = j / ND
       const int d = j % ND, g = (j / ND) >> 1, s2 = (j / ND) & 1;
@@ -532,7 +595,7 @@ __device__ __forceinline__ void pipelined_step(Hook&& hook, const u16* klane, co
   auto mfma = [&](int i) {
     const int j = i >> 1;
     if ((i & 1) == 0) {
-      const int g = j & 1, ks = j >> 1;
+      const int g = j % G, ks = j / G;
       if (ks == 0) s_next[g] = mfma32(op[i], qf[ks], f32x16{});
       else s_next[g] = mfma32(op[i], qf[ks], s_next[g]);
     } else {
@@ -547,9 +610,9 @@ __device__ __forceinline__ void pipelined_step(Hook&& hook, const u16* klane, co
   // rounds each completed pair to bf16, so no instruction waits on the result
   // of the one just before it.  The last two slots' shares are finished after
   // the MFMAs.
-  constexpr int PER = 32 / NM;
-  constexpr int RSP = NM / 4;                 // row-sum MFMAs in slots RSP/2 + j*RSP
-  float arg[32], ex[32];
+  constexpr int PER = NS / NM;
+  constexpr int RSP = NM / (2 * G);           // row-sum MFMAs in slots RSP/2 + j*RSP
+  float arg[NS], ex[NS];
   auto stage_arg = [&](int i) {
 #pragma unroll
     for (int u = 0; u < PER; ++u) {

@@ -182,3 +182,65 @@ def test_search_end_to_end_many_blocks(qkv, oracle_lse_and_mass):
             kth = others[kh - len(tk) - 1]
             for c in set(got.tolist()) ^ exp:
                 assert abs(ref[c] - kth) <= 1e-3 * kth, (h, p, c)
+
+
+def _pair_mode_lists(seed):
+    """Row lists for every pair of query blocks, built so that the two rows of
+    a pair exercise each way the pair kernel can walk them: disjoint rows (no
+    shared block: dual half steps only), shared plus solo blocks with the
+    solo counts on both sides of the 1 : 6 balance rule (dual half steps, or
+    the whole union as full steps with per-half hiding), one row inside the
+    other, identical rows, single solo blocks, and solo runs of 90 to 200
+    blocks that cross several 64-entry windows of the block map, with the
+    ragged last block in one row only."""
+    rng = np.random.default_rng(seed)
+    video = np.arange(len(TB), NB - 1)       # the ragged block only where cat 4 adds it
+
+    def pick(pool, n):
+        return sorted(rng.choice(pool, size=n, replace=False).tolist())
+
+    lists = [None] * NB
+    for P in range((NB + 1) // 2):
+        a_blk, b_blk = 2 * P, 2 * P + 1
+        cat = P % 8
+        if cat == 0:      # disjoint, about 60 solo blocks each
+            s = pick(video, 120)
+            A, B = s[0::2], s[1::2]
+        elif cat in (1, 2):   # 40 shared, A 30 or 29 solo, B 5 solo: 5 * 6 = 30
+            s = pick(video, 75 if cat == 1 else 74)
+            sh, rest = s[:40], s[40:]
+            A, B = sorted(TB + sh + rest[:-5]), sorted(TB + sh + rest[-5:])
+        elif cat == 3:    # B inside A
+            A = sorted(TB + pick(video, 120))
+            B = sorted(rng.choice(A, size=60, replace=False).tolist())
+        elif cat == 4:    # ragged block in A only, long solo runs
+            s = [int(x) for x in pick(video, 190)]
+            A, B = sorted(TB + s[:100] + [NB - 1]), sorted(TB + s[100:])
+        elif cat == 5:    # identical rows
+            A = B = sorted(TB + pick(video, 90))
+        elif cat == 6:    # one solo block each
+            s = pick(video, 2)
+            A, B = sorted(TB + s[:1]), sorted(TB + s[1:])
+        else:             # 200 and 60 solo blocks, some shared
+            s = pick(video, 265)
+            A, B = sorted(s[:5] + s[5:205]), sorted(s[:5] + s[205:])
+        for blk, row in ((a_blk, A), (b_blk, B)):
+            if blk < NB:
+                lists[blk] = list(range(NB)) if blk in TB else [int(x) for x in row]
+    return lists
+
+
+@pytest.mark.parametrize("D", [128, 64])
+def test_pair_walk_modes(D):
+    """Pairs whose rows differ in the ways that select the pair kernel's walk
+    (see _pair_mode_lists), eight consecutive pairs of each kind and the last,
+    single-block pair; both rows of every sampled pair against the oracle."""
+    w = W64.replace(head_dim=D)
+    q, k, v = make_qkv(w, device="cuda")
+    lists = []
+    for h in range(w.heads):
+        lists += _pair_mode_lists(640 + 7 * h + D)
+    rpn, cin = _csr(lists)
+    pairs = list(range(8, 16)) + list(range(96, 104)) + [136]
+    blocks = sorted({b for pr in pairs for b in (2 * pr, 2 * pr + 1) if b < NB})
+    _sparse_vs_oracle(q, k, v, rpn, cin, [blocks] * w.heads, w.scale, f"modes D{D}")
