@@ -52,6 +52,32 @@ def measured_traffic(kind: str):
         return None
 
 
+def library_gemm(sizes=((8192, 20), (16384, 5))):
+    """Square bf16 products through torch.matmul (hipBLASLt): the chip's
+    practical matrix throughput, next to which the attention kernels' share
+    of the 2.5 PFLOP/s peak can be read.  HIP-event mean of `reps` products
+    after three warm-ups."""
+    rows = []
+    for n, reps in sizes:
+        a = torch.randn(n, n, device="cuda", dtype=torch.bfloat16)
+        b = torch.randn(n, n, device="cuda", dtype=torch.bfloat16)
+        for _ in range(3):
+            torch.matmul(a, b)
+        s, e = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        s.record()
+        for _ in range(reps):
+            torch.matmul(a, b)
+        e.record()
+        torch.cuda.synchronize()
+        ms = s.elapsed_time(e) / reps
+        tf = 2.0 * n ** 3 / (ms * 1e-3) / 1e12
+        rows.append({"n": n, "reps": reps, "ms": round(ms, 3), "tflops": round(tf, 1),
+                     "frac_bf16_peak": round(tf / PEAK_BF16_TFLOPS, 4)})
+        print(f"[bench] gemm n={n}: {ms:.3f} ms {tf:.0f} TFLOP/s", file=sys.stderr, flush=True)
+        del a, b
+    return rows
+
+
 def attn_flops(L: int, D: int, H: int, B: int = 1) -> float:
     """QK^T and PV, 2 flops per multiply-add: 4 L^2 D per head."""
     return 4.0 * L * L * D * H * B
@@ -354,9 +380,11 @@ def main():
                     help="sparse block size (the paper's default is 64; the 110K workload uses 128)")
     ap.add_argument("--no-amortised", action="store_true",
                     help="skip the 50-step denoising-loop workload")
-    ap.add_argument("--kernel", choices=["all", "dense", "sparse", "search", "copy"], default="all",
+    ap.add_argument("--kernel", choices=["all", "dense", "sparse", "search", "copy", "gemm"], default="all",
                     help="profile helper: run only one kernel in the timed loop; 'copy' runs a "
-                         "plain 1 GiB device copy, the reference for HBM byte counters")
+                         "plain 1 GiB device copy, the reference for HBM byte counters; 'gemm' "
+                         "times square bf16 library GEMMs (torch.matmul), a reference for the "
+                         "chip's practical matrix throughput")
     args = ap.parse_args()
 
     world = int(os.environ.get("WORLD_SIZE", "1"))
@@ -380,6 +408,11 @@ def main():
             dst.copy_(src)
         torch.cuda.synchronize()
         print(f"[bench] copied {src.numel() * 2} bytes x {max(1, args.steps)}", file=sys.stderr, flush=True)
+        return
+
+    if args.kernel == "gemm":
+        print(json.dumps({"metric": "library bf16 GEMM (torch.matmul), square n x n", "unit": "TFLOP/s",
+                          "rows": library_gemm()}), flush=True)
         return
 
     w = LONG if args.block == LONG.block else LONG.replace(block=args.block, name=LONG.name.replace("_b128", f"_b{args.block}"))
