@@ -30,6 +30,9 @@
  *    memory, keeps a pointer after it returns, or synchronises the device:
  *    each call validates its arguments on the host, enqueues kernels on
  *    `stream` (a hipStream_t; NULL means the default stream) and returns.
+ *    Counters are cleared by kernels, not memsets, so a sequence of calls
+ *    with caller-allocated outputs and workspaces can be captured in a HIP
+ *    graph and replayed.
  *  - Errors: invalid arguments are reported synchronously with a status code
  *    before anything is enqueued.  A failed launch returns ADASPA_ERR_HIP.
  *    A fault inside a kernel surfaces at the caller's next synchronisation.
