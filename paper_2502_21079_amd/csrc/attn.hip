@@ -415,21 +415,26 @@ __global__ __launch_bounds__(64 * NW, NW >= 8 ? 1 : 2) void attn_fwd_kernel(Attn
 // Block-sparse attention with block 64, two query blocks per workgroup.
 //
 // Four waves cover query blocks 2P (waves 0-1) and 2P+1 (waves 2-3), 128
-// rows, and walk the sorted union of the two rows' key-block lists through
-// the same pipeline as attn_fwd_kernel (one 64-key tile per block).  For a
-// tile that only one row keeps, the other half takes its probabilities
+// rows, through the same pipeline as attn_fwd_kernel (one 64-key tile per
+// block).  A byte map in LDS marks which row keeps each key block.  When both
+// rows keep blocks the other does not, in similar numbers, the walk has two
+// phases: the shared blocks as full steps for all 128 rows, then the solo
+// blocks of both rows side by side as 32-key half steps (rows 0-31 of a slot
+// hold a half tile of one row's block, rows 32-63 one of the other's, and
+// each half reads its own rows), so neither half computes on a tile it does
+// not keep.  Otherwise the pair walks the sorted union in ascending order:
+// for a tile that only one row keeps, the other half takes its probabilities
 // against a reference of +inf, so they are exact zeros (exp2(-inf)) and each
 // half accumulates exactly its own tiles, in ascending order, as a one-block
-// workgroup would; that costs one scalar select per step (overwriting the
-// scores with -inf made every step wait for its score MFMAs, ~7%).  A
-// non-finite score in such a tile (an inf or NaN in a key the half does not
-// keep) would still reach the half's sums; it leaves them, or the output
+// workgroup would (this keeps all-blocks-kept bitwise equal to the dense
+// kernel); that costs one scalar select per step (overwriting the scores
+// with -inf made every step wait for its score MFMAs, ~7%).  A non-finite
+// score in such a tile (an inf or NaN in a key the half does not keep)
+// would still reach the half's sums; it leaves them, or the output
 // accumulator, non-finite, which sends the wave to the exact path, where the
-// tile's scores are masked to -inf before the softmax.  Neighbouring
-// query blocks keep mostly the same key blocks, so the union is little larger
-// than each list, and every tile brought into LDS serves 128 rows.  Rows
-// must be strictly ascending lists of blocks in [0, NB); otherwise (or for
-// the ragged last block) tiles are done one at a time with key masking.
+// tile's scores are masked to -inf before the softmax.  Rows must be
+// strictly ascending lists of blocks in [0, NB); otherwise (or for the
+// ragged last block) tiles are done one at a time with key masking.
 // ---------------------------------------------------------------------------
 template <int D, int NW>
 __global__ __launch_bounds__(64 * NW, NW >= 8 ? 1 : 2) void attn_sparse_pair_kernel(AttnParams a) {
