@@ -323,6 +323,70 @@ def denoising_loop(w, tau, search_steps, x0, eps, dense_ref_ms: float, steps: in
     return res
 
 
+HETERO = LONG.replace(name="long_hetero_L110336_H24_d128_b128", head_structure=(0.4, 0.7, 1.0, 1.3),
+                      seed=5)
+
+
+def head_adaptive_comparison(steps: int, w=HETERO, s_bp: int = 9000, tau_bp: int = 9000):
+    """Head-adaptive selection on heads of different concentration (the 110K
+    shape with the shared frame/patch component weighted 0.4 / 0.7 / 1.0 /
+    1.3 across the heads).  From the masses of the fresh LSE: the paper's
+    hierarchical rule at base sparsity s (Sec. 4.2), one uniform keep
+    fraction 1 - s for every head, one uniform fraction at the hierarchical
+    pattern's density, and per-head coverage tau.  For each: density, head
+    Recall (the Sec. 2.3 measure, per head), block-sparse time, and the
+    output's error against dense attention (relative L2 over all rows)."""
+    B, H, L, D, blk = w.batch, w.heads, w.seqlen, w.head_dim, w.block
+    nb = w.nblocks
+    txt = {"text_start": w.text_start, "text_len": w.text_len}
+    print(f"[bench] head-adaptive comparison on {w.name}", file=sys.stderr, flush=True)
+    q, k, v = make_qkv(w, device="cuda")
+    dense_out, lse = ad.dense_attn_lse(q, k, v)
+    res = ad.block_search(q, k, lse, block=blk, mode="coverage", head_param_bp=[tau_bp] * H, **txt)
+    scores = dict(scores=res.block_mass, shape=(B, H, L, D))
+    hier = ad.block_search(None, None, None, block=blk, mode="hierarchical", base_sparsity_bp=s_bp,
+                           recall_threshold_bp=8000, **scores, **txt)
+    dens_h = hier.nnz() / (B * H * nb * nb)
+    same_bp = int(round(10000 * dens_h))
+    pats = {
+        "hierarchical": hier,
+        "uniform_1_minus_s": ad.block_search(None, None, None, block=blk, mode="topk",
+                                             head_param_bp=[10000 - s_bp] * H, **scores, **txt),
+        "uniform_same_density": ad.block_search(None, None, None, block=blk, mode="topk",
+                                                head_param_bp=[same_bp] * H, **scores, **txt),
+        "coverage": res,
+    }
+    out = torch.empty_like(q)
+    dn = torch.linalg.vector_norm(dense_out.float()).item()
+    rec = {"workload": w.name, "head_structure": list(w.head_structure), "base_sparsity": s_bp / 10000,
+           "coverage_tau": tau_bp / 10000}
+    for name, r in pats.items():
+        tm = Timer()
+        for _ in range(2):
+            ad.block_sparse_attn(q, k, v, r.row_ptr, r.col_idx, block=blk, out=out, want_lse=False, **txt)
+        for _ in range(max(3, steps)):
+            tm("s", ad.block_sparse_attn, q, k, v, r.row_ptr, r.col_idx, block=blk, out=out,
+               want_lse=False, **txt)
+        ms = float(np.mean(tm.collect()["s"]))
+        nz = r.nnz()
+        err = torch.linalg.vector_norm(out.float() - dense_out.float()).item() / dn
+        hr = r.head_recall.float().cpu().numpy()[0]
+        hk = r.head_k.cpu().numpy()[0]
+        by_weight = {}
+        for i, g in enumerate(w.head_structure):
+            sel = [h for h in range(H) if h % len(w.head_structure) == i]
+            by_weight[str(g)] = {"k_mean": round(float(np.mean(hk[sel])), 1),
+                                 "recall_mean": round(float(np.mean(hr[sel])), 4)}
+        rec[name] = {"density": round(nz / (B * H * nb * nb), 4), "ms": round(ms, 3),
+                     "tflops": round(sparse_flops(nz, blk, D) / (ms * 1e-3) / 1e12, 1),
+                     "head_recall_mean": round(float(hr.mean()), 4), "head_recall_min": round(float(hr.min()), 4),
+                     "rel_l2_vs_dense": round(err, 5), "by_head_weight": by_weight}
+    rec["uniform_same_density"]["keep_bp"] = same_bp
+    del q, k, v, dense_out, lse, res, pats, out
+    torch.cuda.empty_cache()
+    return rec
+
+
 def length_sweep(block: int, keep_bp: int = 1000, seconds=(4, 8, 12, 16, 24), reps: int = 2):
     """Attention-only scaling: dense vs. block-sparse attention across 720p
     clip lengths (4 latent frames per second of 3,440 patches, 256 text
@@ -555,6 +619,10 @@ def main():
                                     "head_k": [int(x) for x in hk],
                                     "head_recall_mean": round(float(r.head_recall.float().mean().item()), 4)})
 
+    heads_cmp = None
+    if not args.no_sweep and args.kernel == "all":
+        heads_cmp = head_adaptive_comparison(args.steps)
+
     amort = two_phase = None
     if not args.no_amortised and not args.no_sweep:
         del ws
@@ -604,7 +672,7 @@ def main():
                    "step": "dense_attn_lse -> block_search -> block_sparse_attn"},
         "sparse_ms": round(sparse_ms, 3), "dense_ms": round(dense_ms, 3), "search_ms": round(search_ms, 3),
         "search_vs_dense": round(search_ms / dense_ms, 4),
-        "kernels": kernels, "density_sweep": sweep, "amortised_loop": amort,
+        "kernels": kernels, "density_sweep": sweep, "head_adaptive": heads_cmp, "amortised_loop": amort,
         "two_phase_schedule": two_phase, "detail": detail,
         "roofline": roof, "roofline_sparse_keep20": roof_sparse, "cpu_baseline": cpu,
     }

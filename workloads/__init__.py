@@ -17,7 +17,7 @@ one of patch-position vectors ``W[s]`` is drawn, shared by Q, K and V, and
     text token:   X = N_X
 
 with every entry of ``N_X``, ``U`` and ``W`` i.i.d. N(0, 1) and ``N_X``
-independent per tensor.  The result is rounded to bf16 (round to nearest even,
+independent per tensor (``head_structure`` scales the shared part per head).  The result is rounded to bf16 (round to nearest even,
 torch's conversion).  Same-frame keys therefore gain about ``0.64*sqrt(D)`` in
 the scaled score and same-patch keys about ``0.36*sqrt(D)``, which gives the
 frame blocks, diagonals and stripes the paper describes.
@@ -54,6 +54,11 @@ class Workload:
     seed: int
     coverage_bp: int = 9000          # per-head coverage target, basis points
     text_first: bool = True          # text tokens at [0, t) (else at the end)
+    # Per-head weight of the shared frame/patch component, cycled over the
+    # heads (empty: weight 1 for every head).  Unequal weights make heads of
+    # different concentration: a weak structure spreads a row's mass over
+    # many key blocks, a strong one gathers it in the frame and stripe blocks.
+    head_structure: tuple = ()
 
     @property
     def text_start(self) -> int:
@@ -129,6 +134,8 @@ def make_qkv(w: Workload, device="cpu", heads: Optional[range] = None,
             U = torch.randn(w.frames, D, generator=_gen(w.seed, base + 0, device), device=device)
             W = torch.randn(w.patches, D, generator=_gen(w.seed, base + 1, device), device=device)
             shared = 0.8 * U[frame] + 0.6 * W[patch]
+            if w.head_structure:
+                shared *= w.head_structure[h % len(w.head_structure)]
             for ti in range(3):
                 x = torch.randn(L, D, generator=_gen(w.seed, base + 2 + ti, device), device=device)
                 x[v0:v0 + w.video_len] += shared
