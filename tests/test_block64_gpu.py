@@ -3,13 +3,13 @@ paths that need many key blocks: NB = 273 here (a 17,456-token slice of the
 long-video layout: 256 text tokens and five frames of 3,440 patches, ragged
 last block of 48 tokens).
 
-* Block-sparse attention pairs two query blocks per workgroup and walks the
-  sorted union of their lists, reading each list 64 entries at a time through
-  a two-chunk window.  Rows of 137 to 273 entries move that window several
-  times, load chunks at c >= 2 and merge the two lists across chunk
-  boundaries; seeded random lists make the two rows of a pair differ (unions
-  up to the whole row), the oracle's own TOPK selection gives the structured
-  case.
+* Block-sparse attention pairs two query blocks per workgroup: it reads each
+  row's list 64 entries at a time (chunks at c >= 2 for rows of 137 to 273
+  entries) into a byte map of the key blocks, then walks either the shared
+  blocks and the two rows' solo blocks in two phases or the sorted union,
+  streaming the map 64 entries at a time.  Seeded random lists make the two
+  rows of a pair differ (unions up to the whole row), constructed lists take
+  every walk, the oracle's own TOPK selection gives the structured case.
 * The block-mass pass covers four query blocks of 64 per workgroup and writes
   W through a ring of 128 blocks flushed 64 at a time: with NB > 128 the ring
   wraps and flushes inside the loop.
