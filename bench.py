@@ -323,6 +323,43 @@ def denoising_loop(w, tau, search_steps, x0, eps, dense_ref_ms: float, steps: in
     return res
 
 
+def block64_record(q, k, v, lse, w, steps: int, dense_ms: float):
+    """The same inputs at block 64, the paper's default block size (NB = 1,724
+    at 110K): the search from the step's fresh LSE, then block-sparse
+    attention on its coverage pattern and on TOPK 10% / 20%."""
+    B, H, L, D = q.shape
+    nb = (L + 63) // 64
+    txt = {"text_start": w.text_start, "text_len": w.text_len}
+    print("[bench] block 64", file=sys.stderr, flush=True)
+    tm = Timer()
+    res = None
+    for _ in range(1 + max(1, steps // 2)):
+        res = tm("search", ad.block_search, q, k, lse, block=64, mode="coverage",
+                 head_param_bp=[w.coverage_bp] * H, **txt)
+    search_ms = float(np.mean(tm.collect()["search"][1:]))
+    rec = {"nblocks": nb, "search_ms": round(search_ms, 3), "search_vs_dense": round(search_ms / dense_ms, 4)}
+    out = torch.empty_like(q)
+    pats = [("coverage", res)]
+    for name, bp in (("keep10", 1000), ("keep20", 2000)):
+        pats.append((name, ad.block_search(None, None, None, block=64, mode="topk", head_param_bp=[bp] * H,
+                                           scores=res.block_mass, shape=(B, H, L, D), **txt)))
+    for name, r in pats:
+        ts = Timer()
+        for _ in range(2):
+            ad.block_sparse_attn(q, k, v, r.row_ptr, r.col_idx, block=64, out=out, want_lse=False, **txt)
+        for _ in range(max(3, steps)):
+            ts("s", ad.block_sparse_attn, q, k, v, r.row_ptr, r.col_idx, block=64, out=out,
+               want_lse=False, **txt)
+        ms = float(np.mean(ts.collect()["s"]))
+        nz = r.nnz()
+        f = sparse_flops(nz, 64, D) / (ms * 1e-3) / 1e12
+        rec[name] = {"ms": round(ms, 3), "tflops": round(f, 1), "frac_bf16_peak": round(f / PEAK_BF16_TFLOPS, 4),
+                     "density": round(nz / (B * H * nb * nb), 4), "speedup_vs_dense": round(dense_ms / ms, 3)}
+    del res, pats, out
+    torch.cuda.empty_cache()
+    return rec
+
+
 HETERO = LONG.replace(name="long_hetero_L110336_H24_d128_b128", head_structure=(0.4, 0.7, 1.0, 1.3),
                       seed=5)
 
@@ -619,9 +656,11 @@ def main():
                                     "head_k": [int(x) for x in hk],
                                     "head_recall_mean": round(float(r.head_recall.float().mean().item()), 4)})
 
-    heads_cmp = None
+    heads_cmp = b64 = None
     if not args.no_sweep and args.kernel == "all":
         heads_cmp = head_adaptive_comparison(args.steps)
+        if blk == 128:
+            b64 = block64_record(q, k, v, lse, w, args.steps, dense_ms)
 
     amort = two_phase = None
     if not args.no_amortised and not args.no_sweep:
@@ -672,7 +711,8 @@ def main():
                    "step": "dense_attn_lse -> block_search -> block_sparse_attn"},
         "sparse_ms": round(sparse_ms, 3), "dense_ms": round(dense_ms, 3), "search_ms": round(search_ms, 3),
         "search_vs_dense": round(search_ms / dense_ms, 4),
-        "kernels": kernels, "density_sweep": sweep, "head_adaptive": heads_cmp, "amortised_loop": amort,
+        "kernels": kernels, "density_sweep": sweep, "block64": b64, "head_adaptive": heads_cmp,
+        "amortised_loop": amort,
         "two_phase_schedule": two_phase, "detail": detail,
         "roofline": roof, "roofline_sparse_keep20": roof_sparse, "cpu_baseline": cpu,
     }
