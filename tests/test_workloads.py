@@ -57,3 +57,17 @@ def test_head_structure_weights_the_shared_part_only():
         shared = b_[0, :, t:] - z_[0, :, t:]
         torch.testing.assert_close(t_[0, 0, t:] - z_[0, 0, t:], 2.0 * shared[0], rtol=0, atol=1e-5)
         assert torch.equal(t_[0, 1], b_[0, 1])                      # weight 1: the default draw
+
+
+def test_frame_table_must_hold_every_video_token():
+    """A workload whose frames cannot hold its video tokens is refused when it
+    is made, on the host: make_qkv indexes the frame table by v // patches,
+    and on a GPU an index past the table is a memory fault, not an error
+    (L = 777 with 64 text tokens and 178 patches needs a fifth frame)."""
+    import pytest
+    with pytest.raises(ValueError, match="frames"):
+        TINY.replace(head_dim=128, block=64, seqlen=777, patches=178)
+    ok = TINY.replace(head_dim=128, block=64, seqlen=777, frames=5, patches=178)
+    assert (ok.video_len - 1) // ok.patches == ok.frames - 1
+    with pytest.raises(ValueError, match="text_len"):
+        TINY.replace(seqlen=32)

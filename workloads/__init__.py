@@ -60,6 +60,16 @@ class Workload:
     # many key blocks, a strong one gathers it in the frame and stripe blocks.
     head_structure: tuple = ()
 
+    def __post_init__(self):
+        # Every video token must fall in one of the drawn frames: make_qkv
+        # indexes the frame table by v // patches, and on a GPU an index past
+        # the table is a memory fault, not an error.
+        if not (0 <= self.text_len <= self.seqlen):
+            raise ValueError(f"{self.name}: text_len {self.text_len} outside [0, {self.seqlen}]")
+        if self.patches < 1 or self.frames * self.patches < self.seqlen - self.text_len:
+            raise ValueError(f"{self.name}: {self.frames} frames x {self.patches} patches hold fewer "
+                             f"than the {self.seqlen - self.text_len} video tokens")
+
     @property
     def text_start(self) -> int:
         return 0 if self.text_first else self.seqlen - self.text_len
