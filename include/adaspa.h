@@ -16,6 +16,9 @@
  *   adaspa_block_sparse_attn  blockified sparse attention over the selected
  *                             key blocks (Sec. 4.1, bias form with c -> inf)
  *
+ * and adaspa_fused_online_search, the first two in one launch as Algorithm 1
+ * describes them (dense attention + LSE, then the masses of the same rows).
+ *
  * Conventions shared by every call
  * --------------------------------
  *  - Tensors are DEVICE pointers, contiguous, 16-byte aligned.
@@ -174,6 +177,32 @@ adaspa_status adaspa_block_search(const adaspa_problem* prob, const void* q,
                                   int64_t col_capacity, int32_t* head_k,
                                   float* head_recall, void* workspace,
                                   size_t workspace_bytes, void* stream);
+
+/* Fused online search (Algorithm 1, Sec. 4.2): dense attention with LSE and
+ * the block masses of that fresh LSE in ONE kernel launch, then the
+ * selection.  Each workgroup computes the output and LSE of 256 query rows
+ * (first pass) and then the block masses of the same rows (second pass)
+ * while their Q and LSE are still in registers, so Q is read once and the
+ * LSE is not read back.  It produces exactly (bit for bit) what
+ * adaspa_dense_attn_lse followed by adaspa_block_search with that LSE
+ * produces:
+ *   out, lse          as adaspa_dense_attn_lse (lse may be NULL: the masses
+ *                     still use the fresh LSE)
+ *   block_mass, row_ptr, col_idx, head_k, head_recall
+ *                     as adaspa_block_search (ADASPA_F_SCORES_GIVEN is not
+ *                     allowed: ADASPA_ERR_INVALID_ARG)
+ * The workspace, its size (adaspa_block_search_workspace), the capacity
+ * rule, the alignment rules and the errors are those of the two calls; the
+ * workspace also holds the per-XCD work-queue counters of the fused kernel,
+ * which the call clears itself. */
+adaspa_status adaspa_fused_online_search(const adaspa_problem* prob, const void* q,
+                                         const void* k, const void* v, void* out,
+                                         float* lse, const adaspa_select* sel,
+                                         float* block_mass, int32_t* row_ptr,
+                                         int32_t* col_idx, int64_t col_capacity,
+                                         int32_t* head_k, float* head_recall,
+                                         void* workspace, size_t workspace_bytes,
+                                         void* stream);
 
 /* Device bytes of the optional workspace of adaspa_block_sparse_attn (0 for
  * invalid arguments). */

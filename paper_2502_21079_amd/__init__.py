@@ -10,6 +10,9 @@ The three calls mirror the C ABI in ``include/adaspa.h``:
                              (Sec. 4.1 optimal indices, Sec. 4.3 text sink and
                              row-wise uniform selection)
 * :func:`block_sparse_attn`  blockified sparse attention (Sec. 4.1)
+* :func:`fused_online_search`  Algorithm 1 in one launch: dense attention +
+                             LSE and the masses of the same rows, then the
+                             selection (bitwise what the first two give)
 
 There is no CPU fallback: if the library is missing, every call raises.
 """
@@ -25,7 +28,7 @@ import torch
 __all__ = ["dense_attn_lse", "dense_attn_workspace", "block_search", "block_sparse_attn",
            "block_sparse_attn_workspace", "block_sparse_attn_noalloc", "SearchResult",
            "library_path", "load_library", "AdaspaError", "EXPORTED_SYMBOLS",
-           "block_search_workspace", "block_search_capacity"]
+           "block_search_workspace", "block_search_capacity", "fused_online_search"]
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
 _LIB_NAME = "libadaspa.so"
@@ -33,7 +36,8 @@ _LIB_NAME = "libadaspa.so"
 EXPORTED_SYMBOLS = ("adaspa_status_string", "adaspa_dense_attn_workspace", "adaspa_dense_attn_lse",
                     "adaspa_block_search_workspace", "adaspa_block_search_capacity",
                     "adaspa_block_search", "adaspa_block_sparse_attn_workspace",
-                    "adaspa_block_sparse_attn", "adaspa_block_sparse_attn_noalloc")
+                    "adaspa_block_sparse_attn", "adaspa_block_sparse_attn_noalloc",
+                    "adaspa_fused_online_search")
 
 SELECT_TOPK = 0
 SELECT_COVERAGE = 1
@@ -91,6 +95,9 @@ def load_library():
     lib.adaspa_block_search.restype = ctypes.c_int
     lib.adaspa_block_search.argtypes = [P, vp, vp, f32p, S, f32p, i32p, i32p, ctypes.c_int64,
                                         i32p, f32p, vp, ctypes.c_size_t, vp]
+    lib.adaspa_fused_online_search.restype = ctypes.c_int
+    lib.adaspa_fused_online_search.argtypes = [P, vp, vp, vp, vp, f32p, S, f32p, i32p, i32p,
+                                               ctypes.c_int64, i32p, f32p, vp, ctypes.c_size_t, vp]
     lib.adaspa_block_sparse_attn_workspace.restype = ctypes.c_size_t
     lib.adaspa_block_sparse_attn_workspace.argtypes = [P]
     lib.adaspa_block_sparse_attn.restype = ctypes.c_int
@@ -257,32 +264,79 @@ def block_search(q, k, lse, *, block: int, text_start: int, text_len: int,
         _check(lib.adaspa_block_search(ctypes.byref(prob), None, None, None, ctypes.byref(sel),
                                        None, None, None, 0, None, None, None, 0, None))
         raise AdaspaError("invalid block_search arguments")
-    if result is not None:
-        ok = (result.block_mass.shape == (B, H, nb, nb) and result.row_ptr.numel() == B * H * nb + 1
-              and result.col_idx.numel() >= cap and result.head_k.shape == (B, H)
-              and result.block_mass.device == dev and not given)
-        if not ok:
-            raise AdaspaError("result does not fit this search (shape, capacity or device)")
-        mass, row_ptr, col_idx = result.block_mass, result.row_ptr, result.col_idx
-        head_k, head_recall = result.head_k, result.head_recall
-    else:
-        if given:
-            if scores.dtype != torch.float32 or scores.shape != (B, H, nb, nb) or not scores.is_contiguous():
-                raise AdaspaError("scores must be contiguous fp32 [B, H, NB, NB]")
-            mass = scores
-        else:
-            mass = torch.empty(B, H, nb, nb, dtype=torch.float32, device=dev)
-        row_ptr = torch.empty(B * H * nb + 1, dtype=torch.int32, device=dev)
-        col_idx = torch.empty(max(int(cap), 1), dtype=torch.int32, device=dev)
-        head_k = torch.empty(B, H, dtype=torch.int32, device=dev)
-        head_recall = torch.empty(B, H, dtype=torch.float32, device=dev)
+    res = _search_outputs(B, H, nb, cap, dev, result, scores)
     if workspace is None or workspace.numel() < wsb:
         workspace = torch.empty(int(wsb), dtype=torch.uint8, device=dev)
     _check(lib.adaspa_block_search(ctypes.byref(prob), _ptr(q), _ptr(k), _ptr(lse),
-                                   ctypes.byref(sel), _ptr(mass), _ptr(row_ptr), _ptr(col_idx),
-                                   int(col_idx.numel()), _ptr(head_k), _ptr(head_recall),
-                                   _ptr(workspace), int(workspace.numel()), _stream(dev)))
-    return SearchResult(mass, row_ptr, col_idx, head_k, head_recall)
+                                   ctypes.byref(sel), _ptr(res.block_mass), _ptr(res.row_ptr),
+                                   _ptr(res.col_idx), int(res.col_idx.numel()), _ptr(res.head_k),
+                                   _ptr(res.head_recall), _ptr(workspace), int(workspace.numel()),
+                                   _stream(dev)))
+    return res
+
+
+def _search_outputs(B, H, nb, cap, dev, result, scores=None) -> SearchResult:
+    """The outputs of a search: ``result`` checked against the problem, or new
+    tensors (with ``scores`` as the masses when they are given)."""
+    if result is not None:
+        ok = (result.block_mass.shape == (B, H, nb, nb) and result.row_ptr.numel() == B * H * nb + 1
+              and result.col_idx.numel() >= cap and result.head_k.shape == (B, H)
+              and result.block_mass.device == dev and scores is None)
+        if not ok:
+            raise AdaspaError("result does not fit this search (shape, capacity or device)")
+        return result
+    if scores is not None:
+        if scores.dtype != torch.float32 or scores.shape != (B, H, nb, nb) or not scores.is_contiguous():
+            raise AdaspaError("scores must be contiguous fp32 [B, H, NB, NB]")
+        mass = scores
+    else:
+        mass = torch.empty(B, H, nb, nb, dtype=torch.float32, device=dev)
+    return SearchResult(mass, torch.empty(B * H * nb + 1, dtype=torch.int32, device=dev),
+                        torch.empty(max(int(cap), 1), dtype=torch.int32, device=dev),
+                        torch.empty(B, H, dtype=torch.int32, device=dev),
+                        torch.empty(B, H, dtype=torch.float32, device=dev))
+
+
+def fused_online_search(q, k, v, *, block: int, text_start: int, text_len: int, mode: str,
+                        head_param_bp: Optional[Sequence[int]] = None, text_sink: bool = True,
+                        scale: Optional[float] = None, out=None, lse=None, want_lse: bool = True,
+                        workspace: Optional[torch.Tensor] = None, base_sparsity_bp: int = 8000,
+                        recall_threshold_bp: int = 8000,
+                        result: Optional["SearchResult"] = None):
+    """Algorithm 1 (fused online search) in one kernel launch, then the
+    selection: returns (out, lse, SearchResult), bit for bit what
+    :func:`dense_attn_lse` followed by :func:`block_search` with that LSE
+    return.  Arguments as in those two calls; ``lse`` may be skipped
+    (``want_lse=False``) and the masses still use the fresh LSE."""
+    _check_qkv(q, k, v)
+    lib = load_library()
+    B, H, L, D = q.shape
+    dev = q.device
+    nb = (L + block - 1) // block
+    prob = _problem_shape(B, H, L, D, block, text_start, text_len, scale)
+    sel, _keep = _select(mode, head_param_bp, text_sink, False, base_sparsity_bp,
+                         recall_threshold_bp, heads=H)
+    cap = lib.adaspa_block_search_capacity(ctypes.byref(prob), ctypes.byref(sel))
+    wsb = lib.adaspa_block_search_workspace(ctypes.byref(prob), ctypes.byref(sel))
+    if cap < 0 or wsb == 0:
+        _check(lib.adaspa_fused_online_search(ctypes.byref(prob), None, None, None, None, None,
+                                              ctypes.byref(sel), None, None, None, 0, None, None,
+                                              None, 0, None))
+        raise AdaspaError("invalid fused_online_search arguments")
+    if out is None:
+        out = torch.empty_like(q)
+    if lse is None and want_lse:
+        lse = torch.empty(B, H, L, dtype=torch.float32, device=dev)
+    res = _search_outputs(B, H, nb, cap, dev, result)
+    if workspace is None or workspace.numel() < wsb:
+        workspace = torch.empty(int(wsb), dtype=torch.uint8, device=dev)
+    _check(lib.adaspa_fused_online_search(ctypes.byref(prob), _ptr(q), _ptr(k), _ptr(v), _ptr(out),
+                                          _ptr(lse), ctypes.byref(sel), _ptr(res.block_mass),
+                                          _ptr(res.row_ptr), _ptr(res.col_idx),
+                                          int(res.col_idx.numel()), _ptr(res.head_k),
+                                          _ptr(res.head_recall), _ptr(workspace),
+                                          int(workspace.numel()), _stream(dev)))
+    return out, lse, res
 
 
 def block_sparse_attn(q, k, v, row_ptr, col_idx, *, block: int, scale: Optional[float] = None,

@@ -160,6 +160,63 @@ adaspa_status scratch_of_current_device(void** ptr) {
   return ADASPA_OK;
 }
 
+MassParams mass_params(const adaspa_problem* prob, const void* q, const void* k, const float* lse,
+                       float* block_mass) {
+  MassParams m;
+  memset(&m, 0, sizeof m);
+  m.q = (const u16*)q;
+  m.k = (const u16*)k;
+  m.lse = lse;
+  m.w = block_mass;
+  m.batch_heads = prob->batch * prob->heads;
+  m.seqlen = prob->seqlen;
+  m.block = prob->block;
+  m.nkb = num_blocks(prob);
+  m.scale_log2 = scale_of(prob) * 1.4426950408889634f;
+  return m;
+}
+
+// Selection kernels of a checked search (the masses are in block_mass).
+adaspa_status enqueue_selection(const adaspa_problem* prob, const adaspa_select* sel,
+                                float* block_mass, int32_t* row_ptr, int32_t* col_idx,
+                                int32_t* head_k, float* head_recall, void* workspace,
+                                hipStream_t s) {
+  const WsLayout wl = workspace_layout(prob);
+  const int nb = num_blocks(prob);
+  const int bh = prob->batch * prob->heads;
+  SelectParams P;
+  memset(&P, 0, sizeof P);
+  char* ws = (char*)workspace;
+  P.w = block_mass;
+  P.row_ptr = row_ptr;
+  P.col_idx = col_idx;
+  P.head_k_out = head_k;
+  P.head_recall_out = head_recall;
+  P.ws_idx = (int32_t*)(ws + wl.idx);
+  P.ws_prefix = (int64_t*)(ws + wl.prefix);
+  P.ws_curve = (int64_t*)(ws + wl.curve);
+  P.ws_headk = (int32_t*)(ws + wl.headk);
+  P.ws_base = (int64_t*)(ws + wl.base);
+  P.batch_heads = bh;
+  P.heads = prob->heads;
+  P.nb = nb;
+  text_block_range(prob, (sel->flags & ADASPA_F_TEXT_SINK) != 0, &P.text_lo, &P.text_hi);
+  const int n_text = P.text_lo <= P.text_hi ? P.text_hi - P.text_lo + 1 : 0;
+  P.kmin = n_text > 1 ? n_text : 1;
+  P.mode = sel->mode;
+  P.cap = (int64_t)((((uint64_t)1) << 62) / ((uint64_t)nb * (uint64_t)nb));
+  if (sel->mode == ADASPA_SELECT_HIERARCHICAL) {
+    hierarchical_counts(sel->base_sparsity_bp, nb, n_text, &P.k_base, &P.k_hi, &P.k_lo);
+    P.recall_thr_bp = sel->recall_threshold_bp;
+  } else {
+    for (int h = 0; h < prob->heads; ++h)
+      P.head_param[h] = sel->mode == ADASPA_SELECT_TOPK
+                            ? topk_count(sel->head_param_bp[h], nb, n_text)
+                            : sel->head_param_bp[h];
+  }
+  return launch_select(P, s) == hipSuccess ? ADASPA_OK : ADASPA_ERR_HIP;
+}
+
 }  // namespace
 
 
@@ -268,56 +325,56 @@ adaspa_status adaspa_block_search(const adaspa_problem* prob, const void* q, con
     return ADASPA_ERR_WORKSPACE;
 
   hipStream_t s = (hipStream_t)stream;
-  const int nb = num_blocks(prob);
-  const int bh = prob->batch * prob->heads;
   if (!given) {
-    MassParams m;
-    memset(&m, 0, sizeof m);
-    m.q = (const u16*)q;
-    m.k = (const u16*)k;
-    m.lse = lse;
-    m.w = block_mass;
-    m.batch_heads = bh;
-    m.seqlen = prob->seqlen;
-    m.block = prob->block;
-    m.nkb = nb;
-    m.scale_log2 = scale_of(prob) * 1.4426950408889634f;
+    MassParams m = mass_params(prob, q, k, lse, block_mass);
     m.claim = (uint32_t*)((char*)workspace + wl.claim);
     if (launch_block_mass(m, prob->head_dim, s) != hipSuccess) return ADASPA_ERR_HIP;
   }
-
-  SelectParams P;
-  memset(&P, 0, sizeof P);
-  char* ws = (char*)workspace;
-  P.w = block_mass;
-  P.row_ptr = row_ptr;
-  P.col_idx = col_idx;
-  P.head_k_out = head_k;
-  P.head_recall_out = head_recall;
-  P.ws_idx = (int32_t*)(ws + wl.idx);
-  P.ws_prefix = (int64_t*)(ws + wl.prefix);
-  P.ws_curve = (int64_t*)(ws + wl.curve);
-  P.ws_headk = (int32_t*)(ws + wl.headk);
-  P.ws_base = (int64_t*)(ws + wl.base);
-  P.batch_heads = bh;
-  P.heads = prob->heads;
-  P.nb = nb;
-  text_block_range(prob, (sel->flags & ADASPA_F_TEXT_SINK) != 0, &P.text_lo, &P.text_hi);
-  const int n_text = P.text_lo <= P.text_hi ? P.text_hi - P.text_lo + 1 : 0;
-  P.kmin = n_text > 1 ? n_text : 1;
-  P.mode = sel->mode;
-  P.cap = (int64_t)((((uint64_t)1) << 62) / ((uint64_t)nb * (uint64_t)nb));
-  if (sel->mode == ADASPA_SELECT_HIERARCHICAL) {
-    hierarchical_counts(sel->base_sparsity_bp, nb, n_text, &P.k_base, &P.k_hi, &P.k_lo);
-    P.recall_thr_bp = sel->recall_threshold_bp;
-  } else {
-    for (int h = 0; h < prob->heads; ++h)
-      P.head_param[h] = sel->mode == ADASPA_SELECT_TOPK
-                            ? topk_count(sel->head_param_bp[h], nb, n_text)
-                            : sel->head_param_bp[h];
-  }
-  return launch_select(P, s) == hipSuccess ? ADASPA_OK : ADASPA_ERR_HIP;
+  return enqueue_selection(prob, sel, block_mass, row_ptr, col_idx, head_k, head_recall, workspace, s);
 }
+
+adaspa_status adaspa_fused_online_search(const adaspa_problem* prob, const void* q, const void* k,
+                                         const void* v, void* out, float* lse,
+                                         const adaspa_select* sel, float* block_mass,
+                                         int32_t* row_ptr, int32_t* col_idx, int64_t col_capacity,
+                                         int32_t* head_k, float* head_recall, void* workspace,
+                                         size_t workspace_bytes, void* stream) {
+  adaspa_status st = check_problem(prob);
+  if (st != ADASPA_OK) return st;
+  st = check_select(prob, sel);
+  if (st != ADASPA_OK) return st;
+  if (sel->flags & ADASPA_F_SCORES_GIVEN) return ADASPA_ERR_INVALID_ARG;
+  if (!q || !k || !v || !out || !block_mass || !row_ptr || !col_idx) return ADASPA_ERR_INVALID_ARG;
+  if (!aligned16(q) || !aligned16(k) || !aligned16(v) || !aligned16(out) ||
+      (lse && ((uintptr_t)lse & 3u)) || ((uintptr_t)block_mass & 3u) ||
+      ((uintptr_t)row_ptr & 3u) || ((uintptr_t)col_idx & 3u))
+    return ADASPA_ERR_INVALID_ARG;
+  const int64_t need = adaspa_block_search_capacity(prob, sel);
+  if (col_capacity < need) return ADASPA_ERR_CAPACITY;
+  const WsLayout wl = workspace_layout(prob);
+  if (!workspace || workspace_bytes < wl.total || ((uintptr_t)workspace % kAlign))
+    return ADASPA_ERR_WORKSPACE;
+
+  hipStream_t s = (hipStream_t)stream;
+  AttnParams a;
+  memset(&a, 0, sizeof a);
+  a.q = (const u16*)q;
+  a.k = (const u16*)k;
+  a.v = (const u16*)v;
+  a.o = (u16*)out;
+  a.lse = lse;
+  a.batch_heads = prob->batch * prob->heads;
+  a.seqlen = prob->seqlen;
+  a.block = prob->block;
+  a.nkb = num_blocks(prob);
+  a.scale = scale_of(prob);
+  a.scale_log2 = a.scale * 1.4426950408889634f;
+  a.claim = (uint32_t*)((char*)workspace + wl.claim);
+  const MassParams m = mass_params(prob, q, k, lse, block_mass);
+  if (launch_fused_search(a, m, prob->head_dim, s) != hipSuccess) return ADASPA_ERR_HIP;
+  return enqueue_selection(prob, sel, block_mass, row_ptr, col_idx, head_k, head_recall, workspace, s);
+}
+
 
 adaspa_status adaspa_block_sparse_attn(const adaspa_problem* prob, const void* q, const void* k,
                                        const void* v, const int32_t* row_ptr,

@@ -57,10 +57,16 @@ __global__ void claim_reset_kernel(uint32_t* ctr) {
 // reaches past the end of the sequence (and, in a malformed sparse row, any
 // out-of-range block) is done afterwards, one at a time with key masking,
 // which keeps the visiting order of the dense and all-blocks sparse paths the
-// same.
+// same.  After the rows are stored, tail() may continue with the same rows
+// (the fused search below); the attention kernels pass NoTail.
 // ---------------------------------------------------------------------------
-template <int D, int NW, bool SPARSE>
-__global__ __launch_bounds__(64 * NW, NW >= 8 ? 1 : 2) void attn_fwd_kernel(AttnParams a) {
+struct NoTail {
+  template <typename... T>
+  __device__ __forceinline__ void operator()(T&&...) const {}
+};
+
+template <int D, int NW, bool SPARSE, typename Tail>
+__device__ __forceinline__ void attn_fwd_body(AttnParams a, Tail&& tail) {
   constexpr int NT = 64 * NW;
   using KDMA = TileDMA<D, NW, 1>;
   using VDMA = TileDMA<D, NW, 2>;
@@ -409,6 +415,14 @@ __global__ __launch_bounds__(64 * NW, NW >= 8 ? 1 : 2) void attn_fwd_kernel(Attn
     if (hw == 0 && a.lse != nullptr)
       a.lse[(size_t)bh * L + qrow] = lt > 0.f ? fmaf(ref.m, a.scale, logf(lt)) : -INFINITY;
   }
+  // The row's Q fragments, its sum and reference (LSE = m * scale + log lt)
+  // and the K/V ring, which no wave reads any more after the next barrier.
+  tail(bh, qt, qf, lt, ref.m, &sKV[0][0]);
+}
+
+template <int D, int NW, bool SPARSE>
+__global__ __launch_bounds__(64 * NW, NW >= 8 ? 1 : 2) void attn_fwd_kernel(AttnParams a) {
+  attn_fwd_body<D, NW, SPARSE>(a, NoTail{});
 }
 
 // ---------------------------------------------------------------------------
@@ -897,37 +911,26 @@ __global__ __launch_bounds__(64 * NW, NW >= 8 ? 1 : 2) void attn_sparse_pair_ker
 // are combined in a fixed order into an LDS ring per query block, which is
 // written out 64 blocks at a time (coalesced).
 // ---------------------------------------------------------------------------
-template <int D, int QB, int NW>
-__global__ __launch_bounds__(64 * NW, 2) void block_mass_kernel(MassParams a) {
+constexpr int kMassRing = 128;        // blocks of W per row held in LDS before they are written out
+
+// The mass pass of query-block group pg of head bh (QB query blocks, 256
+// rows).  qsrc(qf, nlse2, hoff, qrow, qvalid, hw) supplies this lane's Q
+// fragments and -LSE * log2(e) of its row (-inf for a row past L, whose
+// exp2 terms are then 0); sK0 / sK1 are the two K tile buffers, sRed the
+// per-wave sums of the last two blocks and sW the ring of W blocks not yet
+// written out.
+template <int D, int QB, int NW, typename QSrc>
+__device__ __forceinline__ void block_mass_body(const MassParams& a, int bh, int pg, QSrc&& qsrc,
+                                                u16* sK0, u16* sK1, float (*sRed)[NW],
+                                                float (*sW)[kMassRing]) {
   constexpr int NT = 64 * NW;
   constexpr int WPB = NW / QB;       // waves per query block
   constexpr int SUB = 32 * WPB / KT; // KT-key tiles per key block
   using KDMA = TileDMA<D, NW, 1>;
   constexpr int KS = KDMA::S;
   constexpr int NK = D / 16;
-  __shared__ __attribute__((aligned(1024))) u16 sK0[KDMA::ELEMS];
-  __shared__ __attribute__((aligned(1024))) u16 sK1[KDMA::ELEMS];
-  constexpr int RING = 128, CHUNK = 64;
-  __shared__ float sRed[2][NW];     // per-wave sums of the last two blocks
-  __shared__ float sW[QB][RING];    // blocks of the QB rows of W not yet written out
+  constexpr int RING = kMassRing, CHUNK = 64;
 
-  const int ngrp = (a.nkb + QB - 1) / QB;    // query-block groups per head
-  // One contiguous range of (head, query-block group) items per XCD, through
-  // the per-XCD work queues when a workspace is given (see claim_item).
-  int bh, pg;
-  {
-    int item = (int)blockIdx.x;
-    if (a.claim != nullptr) {
-      __shared__ int s_item;
-      if (threadIdx.x == 0) s_item = claim_item(a.claim, 0, a.n_items);
-      __syncthreads();
-      item = s_item;
-      if (item < 0) return;
-    }
-    const int lid = xcd_remap(item, a.n_items);
-    bh = lid / ngrp;
-    pg = lid % ngrp;
-  }
   const int p0 = pg * QB;           // first query block of the group
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);   // wave-uniform
@@ -940,10 +943,9 @@ __global__ __launch_bounds__(64 * NW, 2) void block_mass_kernel(MassParams a) {
   const bool qvalid = qrow < L;
 
   bf16x8 qf[NK];
-  load_q<D>(a.q + hoff, qrow, L, hw, qf);
+  float nlse2;
+  qsrc(qf, nlse2, hoff, qrow, qvalid, hw);
   const float sl2 = a.scale_log2;
-  // A padding row (past L) gets -inf: exp2 of it is 0 and it adds nothing.
-  const float nlse2 = qvalid ? -a.lse[(size_t)bh * L + qrow] * kLog2e : -INFINITY;
   const int sub = SUB;
   const int nfull = L / KT;   // full key tiles
   float* wrow = a.w + ((size_t)bh * a.nkb + p0) * a.nkb;    // row p0 + qb at wrow + qb * nkb
@@ -1064,6 +1066,74 @@ __global__ __launch_bounds__(64 * NW, 2) void block_mass_kernel(MassParams a) {
     for (int i = flushed + tid; i < a.nkb; i += NT) wrow[(size_t)qb * a.nkb + i] = sW[qb][i % RING];
 }
 
+template <int D, int QB, int NW>
+__global__ __launch_bounds__(64 * NW, 2) void block_mass_kernel(MassParams a) {
+  using KDMA = TileDMA<D, NW, 1>;
+  __shared__ __attribute__((aligned(1024))) u16 sK0[KDMA::ELEMS];
+  __shared__ __attribute__((aligned(1024))) u16 sK1[KDMA::ELEMS];
+  __shared__ float sRed[2][NW];           // per-wave sums of the last two blocks
+  __shared__ float sW[QB][kMassRing];     // blocks of the QB rows of W not yet written out
+
+  const int ngrp = (a.nkb + QB - 1) / QB;    // query-block groups per head
+  // One contiguous range of (head, query-block group) items per XCD, through
+  // the per-XCD work queues when a workspace is given (see claim_item).
+  int bh, pg;
+  {
+    int item = (int)blockIdx.x;
+    if (a.claim != nullptr) {
+      __shared__ int s_item;
+      if (threadIdx.x == 0) s_item = claim_item(a.claim, 0, a.n_items);
+      __syncthreads();
+      item = s_item;
+      if (item < 0) return;
+    }
+    const int lid = xcd_remap(item, a.n_items);
+    bh = lid / ngrp;
+    pg = lid % ngrp;
+  }
+  auto qsrc = [&](bf16x8 (&qf)[D / 16], float& nlse2, size_t hoff, int qrow, bool qvalid, int hw) {
+    load_q<D>(a.q + hoff, qrow, a.seqlen, hw, qf);
+    // A padding row (past L) gets -inf: exp2 of it is 0 and it adds nothing.
+    nlse2 = qvalid ? -a.lse[(size_t)bh * a.seqlen + qrow] * kLog2e : -INFINITY;
+  };
+  block_mass_body<D, QB, NW>(a, bh, pg, qsrc, sK0, sK1, sRed, sW);
+}
+
+// ---------------------------------------------------------------------------
+// Fused online search (Algorithm 1) in one launch.  Each workgroup of eight
+// waves takes 256 query rows of one head: the first pass is the dense
+// attention of those rows (output and LSE, as attn_fwd_kernel<D, 8, false>),
+// the second the block masses of the same rows (QB query blocks of
+// 256 / QB rows, as block_mass_kernel<D, QB, 8>) against that LSE.  The
+// second pass takes each row's Q fragments and LSE from the registers of the
+// first instead of memory (the same lanes hold the same rows in both), and
+// its LDS buffers are carved out of the attention ring, which is free once
+// every wave has passed the barrier after its last read.  Both passes
+// compute exactly what the two separate kernels compute.
+// ---------------------------------------------------------------------------
+template <int D, int QB>
+__global__ __launch_bounds__(512, 1) void fused_search_kernel(AttnParams a, MassParams m) {
+  constexpr int NW = 8;
+  using LD = KVLoader<D, NW>;
+  static_assert(TileDMA<D, NW, 1>::ELEMS <= LD::VOFF, "a mass K tile fits the K part of a ring slot");
+  static_assert((2 * NW + QB * kMassRing) * 4 <= TileDMA<D, NW, 2>::ELEMS * 2,
+                "the mass sums fit the V part of ring slot 0");
+  attn_fwd_body<D, NW, false>(a, [&](int bh, int qt, const bf16x8 (&qf)[D / 16], float lt, float mref,
+                                     u16* ring) {
+    const float lse = lt > 0.f ? fmaf(mref, a.scale, logf(lt)) : -INFINITY;   // as stored
+    __syncthreads();
+    float* sums = reinterpret_cast<float*>(ring + LD::VOFF);
+    auto qsrc = [&](bf16x8 (&q2)[D / 16], float& nlse2, size_t, int, bool qvalid, int) {
+#pragma unroll
+      for (int i = 0; i < D / 16; ++i) q2[i] = qf[i];
+      nlse2 = qvalid ? -lse * kLog2e : -INFINITY;
+    };
+    block_mass_body<D, QB, NW>(m, bh, qt, qsrc, ring, ring + LD::ELEMS,
+                               reinterpret_cast<float (*)[NW]>(sums),
+                               reinterpret_cast<float (*)[kMassRing]>(sums + 2 * NW));
+  });
+}
+
 // ---------------------------------------------------------------------------
 // Launchers
 // ---------------------------------------------------------------------------
@@ -1144,6 +1214,33 @@ static hipError_t launch_mass_t(MassParams a, hipStream_t st) {
     if (e != hipSuccess) return e;
   }
   hipLaunchKernelGGL((block_mass_kernel<D, QB, NW>), dim3(a.n_wg), dim3(64 * NW), 0, st, a);
+  return hipGetLastError();
+}
+
+hipError_t launch_fused_search(AttnParams a, MassParams m, int D, hipStream_t st) {
+  // Work items as in launch_dense: (head, 256-row query tile), which is also
+  // the mass pass's (head, group of 256 / block query blocks).
+  a.row_ptr = nullptr;
+  a.col_idx = nullptr;
+  a.nqt = (a.seqlen + 255) / 256;
+  a.n_items = a.nqt * a.batch_heads;
+  a.n_wg = a.n_items;
+  if (a.claim != nullptr) {
+    a.n_wg = a.n_items + (a.n_items + 3) / 4;
+    hipLaunchKernelGGL(claim_reset_kernel, dim3(1), dim3(64), 0, st, a.claim);
+    const hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+  }
+  m.claim = nullptr;
+  m.n_items = a.n_items;
+  m.n_wg = a.n_wg;
+  if (a.block == 64) {
+    if (D == 64) hipLaunchKernelGGL((fused_search_kernel<64, 4>), dim3(a.n_wg), dim3(512), 0, st, a, m);
+    else hipLaunchKernelGGL((fused_search_kernel<128, 4>), dim3(a.n_wg), dim3(512), 0, st, a, m);
+  } else {
+    if (D == 64) hipLaunchKernelGGL((fused_search_kernel<64, 2>), dim3(a.n_wg), dim3(512), 0, st, a, m);
+    else hipLaunchKernelGGL((fused_search_kernel<128, 2>), dim3(a.n_wg), dim3(512), 0, st, a, m);
+  }
   return hipGetLastError();
 }
 

@@ -78,6 +78,10 @@ struct SelectParams {
 hipError_t launch_dense(AttnParams a, int head_dim, hipStream_t st);
 hipError_t launch_sparse(AttnParams a, int head_dim, hipStream_t st);
 hipError_t launch_block_mass(MassParams a, int head_dim, hipStream_t st);
+// Dense attention + LSE and the block masses of the same rows in one launch
+// (a: the attention's arguments with a.claim the optional work-queue
+// counters; m: the mass pass's, its lse unused).
+hipError_t launch_fused_search(AttnParams a, MassParams m, int head_dim, hipStream_t st);
 hipError_t launch_select(const SelectParams& p, hipStream_t st);
 
 }  // namespace adaspa

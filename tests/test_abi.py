@@ -238,3 +238,32 @@ def test_sparse_noalloc_rejects_bad_arguments(lib):
              None) == 1
     big = _prob(seqlen=64 * 8193, head_dim=64, block=64)
     assert f(ctypes.byref(big), FAKE, FAKE, FAKE, FAKE, FAKE, 10, FAKE, None, None) == 2
+
+
+def test_fused_search_rejects_bad_arguments(lib):
+    """The fused online search takes the arguments of dense attention and the
+    search together and applies both sets of checks, plus one of its own:
+    the masses are always computed (ADASPA_F_SCORES_GIVEN is refused)."""
+    p = _prob()
+    s, _a = _sel()
+    ws = lib.adaspa_block_search_workspace(ctypes.byref(p), ctypes.byref(s))
+    cap = lib.adaspa_block_search_capacity(ctypes.byref(p), ctypes.byref(s))
+
+    def call(**o):
+        return lib.adaspa_fused_online_search(
+            o.get("prob", ctypes.byref(p)), o.get("q", FAKE), FAKE, o.get("v", FAKE), FAKE,
+            o.get("lse", None), o.get("sel", ctypes.byref(s)), FAKE, FAKE, FAKE, o.get("cap", cap),
+            None, None, o.get("ws", FAKE), o.get("wsb", ws), None)
+
+    assert call(v=None) == 1
+    assert call(q=ctypes.c_void_p(0x10008)) == 1
+    assert call(lse=ctypes.c_void_p(0x10002)) == 1
+    assert call(sel=None) == 1
+    given, _b = _sel(flags=1 | 2)
+    assert call(sel=ctypes.byref(given)) == 1
+    assert call(cap=cap - 1) == 3
+    assert call(wsb=ws - 1) == 4
+    assert call(ws=None) == 4
+    assert call(ws=ctypes.c_void_p(0x10010)) == 4
+    assert call(prob=ctypes.byref(_prob(head_dim=96))) == 2
+    assert call(prob=ctypes.byref(_prob(seqlen=0))) == 1
