@@ -360,6 +360,41 @@ def block64_record(q, k, v, lse, w, steps: int, dense_ms: float):
     return rec
 
 
+def fused_search_record(q, k, v, w, steps: int):
+    """Algorithm 1 as one launch (adaspa_fused_online_search: dense attention
+    and LSE of 256 rows, then the masses of the same rows, then the
+    selection) against the same work as two calls (dense attention + LSE,
+    then the search from that LSE), coverage 0.9, at blocks 128 and 64; the
+    two are timed alternately on the same inputs and buffers."""
+    B, H, L, D = q.shape
+    txt = {"text_start": w.text_start, "text_len": w.text_len}
+    out = torch.empty_like(q)
+    lse = torch.empty(B, H, L, dtype=torch.float32, device="cuda")
+    dws = torch.empty(ad.dense_attn_workspace(q.shape), dtype=torch.uint8, device="cuda")
+    rec = {}
+    for blk in (128, 64):
+        print(f"[bench] fused online search, block {blk}", file=sys.stderr, flush=True)
+        tau = [w.coverage_bp] * H
+        kw = dict(block=blk, mode="coverage", head_param_bp=tau, **txt)
+        ws = torch.empty(ad.block_search_workspace(q.shape, blk, w.text_start, w.text_len, "coverage", tau),
+                         dtype=torch.uint8, device="cuda")
+        r2 = ad.block_search(q, k, lse, workspace=ws, **kw)
+        r1 = ad.block_search(q, k, lse, workspace=ws, **kw)
+        tm = Timer()
+        for it in range(1 + max(3, steps)):
+            t = tm if it > 0 else Timer()
+            t("two_calls", lambda: (ad.dense_attn_lse(q, k, v, out=out, lse=lse, workspace=dws),
+                                    ad.block_search(q, k, lse, workspace=ws, result=r2, **kw)))
+            t("fused", ad.fused_online_search, q, k, v, out=out, lse=lse, workspace=ws, result=r1, **kw)
+        ev = {n: float(np.mean(x)) for n, x in tm.collect().items()}
+        rec[f"block{blk}"] = {"fused_ms": round(ev["fused"], 3), "two_calls_ms": round(ev["two_calls"], 3),
+                              "fused_vs_two_calls": round(ev["fused"] / ev["two_calls"], 4)}
+        del ws, r1, r2
+    del out, lse, dws
+    torch.cuda.empty_cache()
+    return rec
+
+
 HETERO = LONG.replace(name="long_hetero_L110336_H24_d128_b128", head_structure=(0.4, 0.7, 1.0, 1.3),
                       seed=5)
 
@@ -481,8 +516,10 @@ def main():
                     help="sparse block size (the paper's default is 64; the 110K workload uses 128)")
     ap.add_argument("--no-amortised", action="store_true",
                     help="skip the 50-step denoising-loop workload")
-    ap.add_argument("--kernel", choices=["all", "dense", "sparse", "search", "copy", "gemm"], default="all",
-                    help="profile helper: run only one kernel in the timed loop; 'copy' runs a "
+    ap.add_argument("--kernel", choices=["all", "dense", "sparse", "search", "fused", "copy", "gemm"],
+                    default="all",
+                    help="profile helper: run only one kernel in the timed loop ('fused': the "
+                         "fused online search, Algorithm 1 in one launch); 'copy' runs a "
                          "plain 1 GiB device copy, the reference for HBM byte counters; 'gemm' "
                          "times square bf16 library GEMMs (torch.matmul), a reference for the "
                          "chip's practical matrix throughput")
@@ -531,6 +568,10 @@ def main():
     torch.cuda.synchronize()
 
     def step(t: Timer):
+        if args.kernel == "fused":
+            return t("fused", ad.fused_online_search, q, k, v, out=out, lse=lse, block=blk,
+                     text_start=w.text_start, text_len=w.text_len, mode="coverage", head_param_bp=tau,
+                     workspace=ws)
         if args.kernel in ("all", "dense"):
             t("dense", ad.dense_attn_lse, q, k, v, out=out, lse=lse)
         res = None
@@ -656,11 +697,12 @@ def main():
                                     "head_k": [int(x) for x in hk],
                                     "head_recall_mean": round(float(r.head_recall.float().mean().item()), 4)})
 
-    heads_cmp = b64 = None
+    heads_cmp = b64 = fused = None
     if not args.no_sweep and args.kernel == "all":
         heads_cmp = head_adaptive_comparison(args.steps)
         if blk == 128:
             b64 = block64_record(q, k, v, lse, w, args.steps, dense_ms)
+        fused = fused_search_record(q, k, v, w, args.steps)
 
     amort = two_phase = None
     if not args.no_amortised and not args.no_sweep:
@@ -712,6 +754,7 @@ def main():
         "sparse_ms": round(sparse_ms, 3), "dense_ms": round(dense_ms, 3), "search_ms": round(search_ms, 3),
         "search_vs_dense": round(search_ms / dense_ms, 4),
         "kernels": kernels, "density_sweep": sweep, "block64": b64, "head_adaptive": heads_cmp,
+        "fused_online_search": fused,
         "amortised_loop": amort,
         "two_phase_schedule": two_phase, "detail": detail,
         "roofline": roof, "roofline_sparse_keep20": roof_sparse, "cpu_baseline": cpu,

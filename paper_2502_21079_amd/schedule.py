@@ -33,7 +33,7 @@ import torch
 
 from . import (AdaspaError, SearchResult, block_search, block_search_workspace,
                block_sparse_attn, block_sparse_attn_workspace, dense_attn_lse,
-               dense_attn_workspace)
+               dense_attn_workspace, fused_online_search)
 
 __all__ = ["DENSE", "FUSED_SEARCH", "CACHED_SEARCH", "SPARSE", "SearchSchedule",
            "AdaSpaAttention"]
@@ -85,7 +85,12 @@ class AdaSpaAttention:
     ``step(t, q, k, v)`` makes the call the schedule names for step t and
     returns the attention output; the LSE of the fused search and the
     current block pattern persist between steps.  ``shape`` is (B, H, L, D);
-    the selection arguments are those of :func:`block_search`."""
+    the selection arguments are those of :func:`block_search`.  With
+    ``fused_kernel`` the fused search step runs Algorithm 1 as one launch
+    (:func:`fused_online_search`), otherwise as dense attention followed by
+    the search; the results are bitwise the same, and on MI355X the two
+    launches are the faster of the two (the fused kernel's mass pass runs at
+    the attention pass's two waves per SIMD instead of four)."""
     shape: Tuple[int, int, int, int]
     block: int
     text_start: int
@@ -97,6 +102,7 @@ class AdaSpaAttention:
     schedule: SearchSchedule = field(default_factory=SearchSchedule)
     scale: Optional[float] = None
     device: str = "cuda"
+    fused_kernel: bool = False
 
     def __post_init__(self):
         B, H, L, D = self.shape
@@ -132,10 +138,17 @@ class AdaSpaAttention:
                            workspace=self._ws_dense)
             return out, a
         if a == FUSED_SEARCH:
-            dense_attn_lse(q, k, v, scale=self.scale, out=out, lse=self.lse,
-                           workspace=self._ws_dense)
+            if self.fused_kernel:
+                _, _, self.search = fused_online_search(
+                    q, k, v, block=self.block, text_start=self.text_start, text_len=self.text_len,
+                    mode=self.mode, head_param_bp=self.head_param_bp, scale=self.scale, out=out,
+                    lse=self.lse, workspace=self._ws_search, base_sparsity_bp=self.base_sparsity_bp,
+                    recall_threshold_bp=self.recall_threshold_bp, result=self.search)
+            else:
+                dense_attn_lse(q, k, v, scale=self.scale, out=out, lse=self.lse,
+                               workspace=self._ws_dense)
+                self._search(q, k)
             self.lse_step = t
-            self._search(q, k)
             self.search_step = t
             return out, a
         if self.search is None:

@@ -54,13 +54,17 @@ def _check_lists(res, sel, W, w):
     return same
 
 
-def test_two_phase_schedule_against_oracle():
+@pytest.mark.parametrize("fused_kernel", [False, True])
+def test_two_phase_schedule_against_oracle(fused_kernel):
+    """Both ways of running the fused search step: dense attention then the
+    search, or Algorithm 1 as one launch."""
     w = TINY
     x0 = make_qkv(w, device="cuda", fp32=True)
     eps = make_drift_noise(w, device="cuda", seed=4)
     layer = AdaSpaAttention((w.batch, w.heads, w.seqlen, w.head_dim), block=w.block,
                             text_start=w.text_start, text_len=w.text_len, mode="topk",
-                            head_param_bp=[KEEP] * w.heads, schedule=SearchSchedule((2, 5)))
+                            head_param_bp=[KEEP] * w.heads, schedule=SearchSchedule((2, 5)),
+                            fused_kernel=fused_kernel)
     nb = w.nblocks
     lse2 = None            # the oracle's LSE of the fused-search step (per head)
     pattern = None         # the oracle's current pattern
