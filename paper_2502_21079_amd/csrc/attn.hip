@@ -401,20 +401,12 @@ __device__ __forceinline__ void attn_fwd_body(AttnParams a, Tail&& tail) {
     lt = lo + hi;
   }
   const float inv = lt > 0.f ? 1.f / lt : 0.f;
-  if (qrow < L) {
-    u16* orow = a.o + hoff + (size_t)qrow * D;
-#pragma unroll
-    for (int d = 0; d < ND; ++d)
-#pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        bf16x4 w;
-#pragma unroll
-        for (int j = 0; j < 4; ++j) w[j] = (__bf16)(o[d][4 * i + j] * inv);
-        *reinterpret_cast<bf16x4*>(orow + d * 32 + 8 * i + 4 * hw) = w;
-      }
-    if (hw == 0 && a.lse != nullptr)
-      a.lse[(size_t)bh * L + qrow] = lt > 0.f ? fmaf(ref.m, a.scale, logf(lt)) : -INFINITY;
-  }
+  // Every wave's tile loads have landed and its reads of the ring are done.
+  static_assert(kStageElems<D, NW> <= RING * LD::ELEMS, "the output tiles fit the ring");
+  __syncthreads();
+  store_rows<D>(o, inv, &sKV[0][0] + wave * 32 * (D + 8), a.o + hoff, qt * (32 * NW) + wave * 32, L, lane);
+  if (qrow < L && hw == 0 && a.lse != nullptr)
+    a.lse[(size_t)bh * L + qrow] = lt > 0.f ? fmaf(ref.m, a.scale, logf(lt)) : -INFINITY;
   // The row's Q fragments, its sum and reference (LSE = m * scale + log lt)
   // and the K/V ring, which no wave reads any more after the next barrier.
   tail(bh, qt, qf, lt, ref.m, &sKV[0][0]);
@@ -878,20 +870,12 @@ __global__ __launch_bounds__(64 * NW, NW >= 8 ? 1 : 2) void attn_sparse_pair_ker
     lt = lo + hi;
   }
   const float inv = lt > 0.f ? 1.f / lt : 0.f;
-  if (qrow < L) {
-    u16* orow = a.o + hoff + (size_t)qrow * D;
-#pragma unroll
-    for (int d = 0; d < ND; ++d)
-#pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        bf16x4 w;
-#pragma unroll
-        for (int j = 0; j < 4; ++j) w[j] = (__bf16)(o[d][4 * i + j] * inv);
-        *reinterpret_cast<bf16x4*>(orow + d * 32 + 8 * i + 4 * hw) = w;
-      }
-    if (hw == 0 && a.lse != nullptr)
-      a.lse[(size_t)bh * L + qrow] = lt > 0.f ? fmaf(ref.m, a.scale, logf(lt)) : -INFINITY;
-  }
+  // As in attn_fwd_body: the output tiles go out through the free ring.
+  static_assert(kStageElems<D, NW> <= 2 * LD::ELEMS, "the output tiles fit the ring");
+  __syncthreads();
+  store_rows<D>(o, inv, &sKV[0][0] + wave * 32 * (D + 8), a.o + hoff, pq * (2 * BLK) + wave * 32, L, lane);
+  if (qrow < L && hw == 0 && a.lse != nullptr)
+    a.lse[(size_t)bh * L + qrow] = lt > 0.f ? fmaf(ref.m, a.scale, logf(lt)) : -INFINITY;
 }
 
 // ---------------------------------------------------------------------------

@@ -550,6 +550,36 @@ __device__ __forceinline__ void pv_tile(const u16* vlane, const bf16x8 (&pb)[2][
       }
 }
 
+// Writes one wave's 32 x D output tile (o scaled by inv, rounded to bf16) as
+// whole rows: the tile goes through stage, this wave's region of the K/V ring
+// (32 rows of D + 8 elements, free once every wave has passed a barrier
+// after its last use of the ring), and each store instruction then writes
+// 64 / (D / 8) complete rows of 2 D bytes instead of 8-byte pieces of 32
+// rows.  Row row0 + r of out gets tile row r; rows at or past L are skipped.
+template <int D>
+__device__ __forceinline__ void store_rows(const f32x16 (&o)[D / 32], float inv, u16* stage, u16* out,
+                                           int row0, int L, int lane) {
+  constexpr int ND = D / 32, RS = D + 8, CPR = D / 8, RPI = 64 / CPR;
+  const int hw = lane >> 5, c32 = lane & 31;
+#pragma unroll
+  for (int d = 0; d < ND; ++d)
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      bf16x4 w;
+#pragma unroll
+      for (int j = 0; j < 4; ++j) w[j] = (__bf16)(o[d][4 * i + j] * inv);
+      *reinterpret_cast<bf16x4*>(stage + c32 * RS + d * 32 + 8 * i + 4 * hw) = w;
+    }
+#pragma unroll
+  for (int j = 0; j < 32 / RPI; ++j) {
+    const int r = lane / CPR + RPI * j;
+    const bf16x8 v = *reinterpret_cast<const bf16x8*>(stage + r * RS + (lane % CPR) * 8);
+    if (row0 + r < L) *reinterpret_cast<bf16x8*>(out + (size_t)(row0 + r) * D + (lane % CPR) * 8) = v;
+  }
+}
+template <int D, int NW>
+constexpr int kStageElems = NW * 32 * (D + 8);    // ring elements store_rows uses
+
 // One pipelined step, scheduled by hand: NM = 2*NK + 4*ND MFMA slots that
 // alternate a QK MFMA (scores of the next tile) and a PV MFMA (output update
 // of the previous tile).  The QK MFMAs alternate between the two 32-key score
