@@ -613,7 +613,11 @@ def main():
         res = step(timer)
     torch.cuda.synchronize()
     wall_ms = (time.perf_counter() - t0) * 1e3 / args.steps
-    ev = {kname: float(np.mean(v_)) for kname, v_ in timer.collect().items()}
+    samples = timer.collect()
+    ev = {kname: float(np.mean(v_)) for kname, v_ in samples.items()}
+    spread = {kname: {"median": round(float(np.median(v_)), 3), "p10": round(float(np.percentile(v_, 10)), 3),
+                      "p90": round(float(np.percentile(v_, 90)), 3), "n": len(v_)}
+              for kname, v_ in samples.items()}
     print(f"[bench] step ms {wall_ms:.2f} kernels {ev}", file=sys.stderr, flush=True)
     if args.kernel != "all":
         return
@@ -627,12 +631,14 @@ def main():
     dense_ms, search_ms, sparse_ms = ev["dense"], ev["search"], ev["sparse"]
     tf = lambda f, ms: f / (ms * 1e-3) / 1e12
     kernels = {
-        "dense_attn_lse": {"ms": round(dense_ms, 3), "tflops": round(tf(f_dense, dense_ms), 1),
+        "dense_attn_lse": {"ms": round(dense_ms, 3), "ms_spread": spread["dense"],
+                           "tflops": round(tf(f_dense, dense_ms), 1),
                            "frac_bf16_peak": round(tf(f_dense, dense_ms) / PEAK_BF16_TFLOPS, 4)},
-        "block_search": {"ms": round(search_ms, 3),
+        "block_search": {"ms": round(search_ms, 3), "ms_spread": spread["search"],
                          "mass_tflops_equiv": round(tf(f_mass, search_ms), 1),
                          "vs_dense": round(search_ms / dense_ms, 4)},
-        "block_sparse_attn": {"ms": round(sparse_ms, 3), "tflops": round(tf(f_sparse, sparse_ms), 1),
+        "block_sparse_attn": {"ms": round(sparse_ms, 3), "ms_spread": spread["sparse"],
+                              "tflops": round(tf(f_sparse, sparse_ms), 1),
                               "frac_bf16_peak": round(tf(f_sparse, sparse_ms) / PEAK_BF16_TFLOPS, 4),
                               "target_frac": SPARSE_TARGET_FRAC,
                               "target_met": tf(f_sparse, sparse_ms) / PEAK_BF16_TFLOPS >= SPARSE_TARGET_FRAC,
