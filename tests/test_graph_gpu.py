@@ -2,7 +2,8 @@
 validates its arguments and enqueues kernels (its work-queue counters are
 cleared by a kernel, not a memset), so one denoising step of the search
 schedule (dense attention + LSE, block search, block-sparse attention on the
-new pattern) can be captured once and replayed.  Between replays new seeded
+new pattern; or the fused online search, then block-sparse attention) can be
+captured once and replayed.  Between replays new seeded
 inputs are written into the captured buffers and the same step runs eagerly
 into separate buffers; every replay must equal the eager step bit for bit."""
 import pytest
@@ -20,10 +21,13 @@ CASES = {
 
 
 class Step:
-    """One search step with every output and workspace allocated up front."""
+    """One search step with every output and workspace allocated up front;
+    with ``fused`` the dense pass and the masses run as one launch (the fused
+    online search)."""
 
-    def __init__(self, w, q, k, v):
+    def __init__(self, w, q, k, v, fused=False):
         self.w, self.q, self.k, self.v = w, q, k, v
+        self.fused = fused
         B, H, L, D = q.shape
         self.kw = dict(block=w.block, text_start=w.text_start, text_len=w.text_len)
         self.tau = [9000] * H
@@ -40,9 +44,14 @@ class Step:
         self.res = None
 
     def __call__(self):
-        ad.dense_attn_lse(self.q, self.k, self.v, out=self.out_d, lse=self.lse, workspace=self.ws_d)
-        self.res = ad.block_search(self.q, self.k, self.lse, mode="coverage", head_param_bp=self.tau,
-                                   workspace=self.ws_s, result=self.res, **self.kw)
+        if self.fused:
+            _, _, self.res = ad.fused_online_search(self.q, self.k, self.v, mode="coverage",
+                                                    head_param_bp=self.tau, out=self.out_d, lse=self.lse,
+                                                    workspace=self.ws_s, result=self.res, **self.kw)
+        else:
+            ad.dense_attn_lse(self.q, self.k, self.v, out=self.out_d, lse=self.lse, workspace=self.ws_d)
+            self.res = ad.block_search(self.q, self.k, self.lse, mode="coverage", head_param_bp=self.tau,
+                                       workspace=self.ws_s, result=self.res, **self.kw)
         ad.block_sparse_attn(self.q, self.k, self.v, self.res.row_ptr, self.res.col_idx, out=self.out_s,
                              lse=self.lse_s, workspace=self.ws_p, **self.kw)
 
@@ -53,11 +62,12 @@ class Step:
                 "recall": self.res.head_recall, "sparse_out": self.out_s, "sparse_lse": self.lse_s}
 
 
+@pytest.mark.parametrize("fused", [False, True])
 @pytest.mark.parametrize("case", sorted(CASES))
-def test_step_graph_replays_equal_eager(case):
+def test_step_graph_replays_equal_eager(case, fused):
     w = CASES[case]
     q, k, v = (t.contiguous() for t in make_qkv(w, device="cuda"))
-    cap = Step(w, q, k, v)
+    cap = Step(w, q, k, v, fused)
     side = torch.cuda.Stream()
     side.wait_stream(torch.cuda.current_stream())
     with torch.cuda.stream(side):
@@ -78,7 +88,7 @@ def test_step_graph_replays_equal_eager(case):
         g.replay()
         torch.cuda.synchronize()
         got = {name: t.clone() for name, t in cap.outputs().items()}
-        ref = Step(w, qn.contiguous(), kn.contiguous(), vn.contiguous())
+        ref = Step(w, qn.contiguous(), kn.contiguous(), vn.contiguous(), fused)
         ref()
         torch.cuda.synchronize()
         want = ref.outputs()
