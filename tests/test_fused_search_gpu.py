@@ -122,3 +122,29 @@ def test_fused_extreme_scores_equal_separate_calls(kind, D, block, L):
     kw = dict(block=block, text_start=0, text_len=0, mode="topk", head_param_bp=[5000, 5000],
               scale=scale)
     _assert_same(ad.fused_online_search(q, k, v, **kw), _separate(q, k, v, **kw))
+
+
+@pytest.mark.parametrize("D,block,L", [(128, 64, 1), (64, 128, 1), (64, 64, 64), (128, 128, 130),
+                                       (128, 64, 130)])
+def test_degenerate_lengths(D, block, L):
+    """Lengths of one token, exactly one block, and one block plus two rows:
+    the mass pass (no full key tile, or one, and a ragged last tile) against
+    the oracle given the same fp32 LSE, and the fused search equal to the two
+    calls bit for bit."""
+    T = min(64, L)
+    w = TINY.replace(head_dim=D, block=block, seqlen=L, text_len=T, frames=4,
+                     patches=max(1, (L - T + 3) // 4))
+    q, k, v = make_qkv(w, device="cuda")
+    H = w.heads
+    lse_ref = torch.empty(1, H, L, dtype=torch.float32)
+    for h in range(H):
+        _, l_ref = oracle.dense_attention(f64(q[0, h]), f64(k[0, h]), f64(v[0, h]), w.scale)
+        lse_ref[0, h] = torch.from_numpy(l_ref.astype(np.float32))
+    res = ad.block_search(q, k, lse_ref.cuda(), block=block, text_start=0, text_len=T, mode="topk",
+                          head_param_bp=[5000] * H)
+    torch.cuda.synchronize()
+    for h in range(H):
+        ref = oracle.block_mass(f64(q[0, h]), f64(k[0, h]), f64(lse_ref[0, h]), w.scale, block)
+        check_mass(res.block_mass[0, h], ref, f"L{L} h{h}")
+    kw = dict(block=block, text_start=0, text_len=T, mode="coverage", head_param_bp=[9000] * H)
+    _assert_same(ad.fused_online_search(q, k, v, **kw), _separate(q, k, v, **kw))
