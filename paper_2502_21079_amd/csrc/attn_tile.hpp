@@ -570,7 +570,7 @@ __device__ __forceinline__ void store_rows(const f32x16 (&o)[D / 32], float inv,
       for (int j = 0; j < 4; ++j) w[j] = (__bf16)(o[d][4 * i + j] * inv);
       *reinterpret_cast<bf16x4*>(stage + c32 * RS + d * 32 + 8 * i + 4 * hw) = w;
     }
-#pragma unroll
+#pragma unroll 4
   for (int j = 0; j < 32 / RPI; ++j) {
     const int r = lane / CPR + RPI * j;
     const bf16x8 v = *reinterpret_cast<const bf16x8*>(stage + r * RS + (lane % CPR) * 8);
