@@ -142,6 +142,19 @@ def _check_qkv(*ts):
             raise AdaspaError(f"shape mismatch {tuple(t.shape)} vs {tuple(ref.shape)}")
 
 
+def _check_outputs(q, out, lse):
+    """Caller-provided outputs must have the shapes the kernels write: the
+    library sees only pointers, so a smaller buffer would be written past its
+    end on the device."""
+    B, H, L, D = q.shape
+    if out is not None and (out.dtype != torch.bfloat16 or tuple(out.shape) != (B, H, L, D)
+                            or not out.is_contiguous() or out.device != q.device):
+        raise AdaspaError(f"out must be a contiguous bf16 [B, H, L, D] = {(B, H, L, D)} tensor on q's device")
+    if lse is not None and (lse.dtype != torch.float32 or tuple(lse.shape) != (B, H, L)
+                            or not lse.is_contiguous() or lse.device != q.device):
+        raise AdaspaError(f"lse must be a contiguous fp32 [B, H, L] = {(B, H, L)} tensor on q's device")
+
+
 def _select(mode: str, head_param_bp: Optional[Sequence[int]], text_sink: bool,
             scores_given: bool, base_sparsity_bp: int = 8000, recall_threshold_bp: int = 8000,
             heads: Optional[int] = None):
@@ -170,6 +183,7 @@ def dense_attn_lse(q, k, v, *, scale: Optional[float] = None, out=None, lse=None
     given); ``balance=False`` splits the work statically.  The results are
     the same either way."""
     _check_qkv(q, k, v)
+    _check_outputs(q, out, lse)
     lib = load_library()
     B, H, L, D = q.shape
     if out is None:
@@ -323,6 +337,7 @@ def fused_online_search(q, k, v, *, block: int, text_start: int, text_len: int, 
                                               ctypes.byref(sel), None, None, None, 0, None, None,
                                               None, 0, None))
         raise AdaspaError("invalid fused_online_search arguments")
+    _check_outputs(q, out, lse)
     if out is None:
         out = torch.empty_like(q)
     if lse is None and want_lse:
@@ -359,6 +374,7 @@ def block_sparse_attn(q, k, v, row_ptr, col_idx, *, block: int, scale: Optional[
             raise AdaspaError("row_ptr and col_idx must be contiguous int32 on q's device")
     if row_ptr.numel() != B * H * nb + 1:
         raise AdaspaError(f"row_ptr must have B*H*NB+1 = {B * H * nb + 1} entries")
+    _check_outputs(q, out, lse)
     if out is None:
         out = torch.empty_like(q)
     if lse is None and want_lse:
@@ -404,9 +420,7 @@ def block_sparse_attn_noalloc(q, k, v, row_ptr, col_idx, *, block: int, out, lse
             raise AdaspaError("row_ptr and col_idx must be contiguous int32 on q's device")
     if row_ptr.numel() != B * H * nb + 1:
         raise AdaspaError(f"row_ptr must have B*H*NB+1 = {B * H * nb + 1} entries")
-    if lse is not None and (lse.dtype != torch.float32 or lse.shape != (B, H, L)
-                            or not lse.is_contiguous() or lse.device != q.device):
-        raise AdaspaError("lse must be contiguous fp32 [B, H, L] on q's device")
+    _check_outputs(q, out, lse)
     prob = _problem(q, block, text_start, text_len, scale)
     _check(lib.adaspa_block_sparse_attn_noalloc(ctypes.byref(prob), _ptr(q), _ptr(k), _ptr(v),
                                                 _ptr(row_ptr), _ptr(col_idx), int(col_idx.numel()),

@@ -267,3 +267,22 @@ def test_fused_search_rejects_bad_arguments(lib):
     assert call(ws=ctypes.c_void_p(0x10010)) == 4
     assert call(prob=ctypes.byref(_prob(head_dim=96))) == 2
     assert call(prob=ctypes.byref(_prob(seqlen=0))) == 1
+
+
+def test_binding_checks_caller_outputs():
+    """The binding refuses caller-provided outputs whose dtype, shape or
+    layout differ from what the kernels write (the library sees pointers
+    only): checked on the host, before any call."""
+    import torch
+    q = torch.empty(1, 2, 8, 64, dtype=torch.bfloat16)
+    ad._check_outputs(q, torch.empty_like(q), torch.empty(1, 2, 8, dtype=torch.float32))
+    ad._check_outputs(q, None, None)
+    bad_out = [torch.empty(1, 2, 7, 64, dtype=torch.bfloat16), torch.empty(1, 2, 8, 64, dtype=torch.float32),
+               torch.empty(1, 2, 64, 8, dtype=torch.bfloat16).transpose(2, 3)]
+    for o in bad_out:
+        with pytest.raises(ad.AdaspaError, match="out must"):
+            ad._check_outputs(q, o, None)
+    for l in [torch.empty(1, 2, 7, dtype=torch.float32), torch.empty(1, 2, 8, dtype=torch.bfloat16),
+              torch.empty(2, 8, dtype=torch.float32)]:
+        with pytest.raises(ad.AdaspaError, match="lse must"):
+            ad._check_outputs(q, None, l)
