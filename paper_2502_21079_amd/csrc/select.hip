@@ -87,18 +87,18 @@ __global__ __launch_bounds__(SEL_NT) void select_rank_kernel(SelectParams P) {
     keys[i] = kk;
   }
   __syncthreads();
-  // Bitonic sort, descending.
+  // Bitonic sort, descending.  Each stage visits its n / 2 compare-exchange
+  // pairs (i, i + j) directly: i has bit j clear.
   for (int k = 2; k <= n; k <<= 1) {
     for (int j = k >> 1; j > 0; j >>= 1) {
-      for (int i = tid; i < n; i += SEL_NT) {
-        int ixj = i ^ j;
-        if (ixj > i) {
-          uint64_t x = keys[i], y = keys[ixj];
-          bool desc = (i & k) == 0;
-          if (desc ? (x < y) : (x > y)) {
-            keys[i] = y;
-            keys[ixj] = x;
-          }
+      for (int pr = tid; pr < (n >> 1); pr += SEL_NT) {
+        const int i = ((pr & ~(j - 1)) << 1) | (pr & (j - 1));
+        const int ixj = i + j;
+        uint64_t x = keys[i], y = keys[ixj];
+        bool desc = (i & k) == 0;
+        if (desc ? (x < y) : (x > y)) {
+          keys[i] = y;
+          keys[ixj] = x;
         }
       }
       __syncthreads();
