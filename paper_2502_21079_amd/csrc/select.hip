@@ -63,6 +63,9 @@ __global__ __launch_bounds__(SEL_NT) void select_rank_kernel(SelectParams P) {
   int64_t* pref = P.ws_prefix + (size_t)row * nb;
   int32_t* ord = P.ws_idx + (size_t)row * nb;
   const int per = (nb + SEL_NT - 1) / SEL_NT;   // contiguous chunk per thread
+  // The curve (B*H*nb entries, one per row) is summed with atomics by the
+  // next kernel: clear it here.
+  if (tid == 0) P.ws_curve[row] = 0;
 
   if (in_text(p, P.text_lo, P.text_hi)) {
     int64_t s = 0;
@@ -127,16 +130,24 @@ __global__ __launch_bounds__(SEL_NT) void select_rank_kernel(SelectParams P) {
   }
 }
 
-// kept(k) of each head for k = 1..nb: sum over the head's rows.
+// kept(k) of each head for k = 1..nb: sum over the head's rows.  Workgroup
+// (x, bh, z) sums rows [z nb / CURVE_SPLIT, (z + 1) nb / CURVE_SPLIT) and adds
+// its partial sums to the curve with 64-bit integer atomics (exact, so the
+// result does not depend on their order).
+constexpr int CURVE_SPLIT = 8;
 __global__ __launch_bounds__(SEL_NT) void select_curve_kernel(SelectParams P) {
   const int bh = blockIdx.y;
   const int k1 = blockIdx.x * SEL_NT + threadIdx.x;
   const int nb = P.nb;
   if (k1 >= nb) return;
+  const int p0 = (int)((int64_t)blockIdx.z * nb / CURVE_SPLIT);
+  const int p1 = (int)((int64_t)(blockIdx.z + 1) * nb / CURVE_SPLIT);
   const int64_t* base = P.ws_prefix + (size_t)bh * nb * nb + k1;
   int64_t s = 0;
-  for (int p = 0; p < nb; ++p) s += base[(size_t)p * nb];
-  P.ws_curve[(size_t)bh * nb + k1] = s;
+  for (int p = p0; p < p1; ++p) s += base[(size_t)p * nb];
+  if (p1 > p0)
+    atomicAdd(reinterpret_cast<unsigned long long*>(P.ws_curve + (size_t)bh * nb + k1),
+              (unsigned long long)s);
 }
 
 // Per-head count, Recall and the first col_idx entry of every head.
@@ -243,7 +254,7 @@ hipError_t launch_select(const SelectParams& P, hipStream_t st) {
   int n = 1;
   while (n < P.nb) n <<= 1;
   hipLaunchKernelGGL(select_rank_kernel, dim3(rows), dim3(SEL_NT), (size_t)n * sizeof(uint64_t), st, P);
-  hipLaunchKernelGGL(select_curve_kernel, dim3((P.nb + SEL_NT - 1) / SEL_NT, P.batch_heads),
+  hipLaunchKernelGGL(select_curve_kernel, dim3((P.nb + SEL_NT - 1) / SEL_NT, P.batch_heads, CURVE_SPLIT),
                      dim3(SEL_NT), 0, st, P);
   hipLaunchKernelGGL(select_heads_kernel, dim3(1), dim3(SEL_NT), 0, st, P);
   hipLaunchKernelGGL(select_emit_kernel, dim3(rows), dim3(SEL_NT), 0, st, P);
