@@ -37,6 +37,13 @@ PEAK_HBM_GBS = 8000.0
 # Goal for block-sparse attention: effective FLOP/s over the kept blocks at
 # half the dense bf16 MFMA peak.  The JSON line says whether it is met.
 SPARSE_TARGET_FRAC = 0.5
+# Vector ALU of the block-mass pass: 256 CUs x 4 SIMDs x 16 lanes of full-rate
+# (unpacked) fp32 instructions per clock at 2.4 GHz, the basis of the 157.3
+# TFLOP/s fp32 vector figure (which counts packed FMAs).  Each score takes one
+# FMA, one exponential (v_exp_f32 issues at half that rate) and one add: four
+# full-rate slots.
+VALU_LANE_OPS_PER_S = 256 * 4 * 16 * 2.4e9
+MASS_SLOTS_PER_SCORE = 4
 
 
 def measured_traffic(kind: str):
@@ -645,6 +652,23 @@ def main():
                               "nnz_blocks": nnz, "density": round(nnz / (B * H * nb * nb), 5),
                               "speedup_vs_dense": round(dense_ms / sparse_ms, 3)},
     }
+    # the mass pass alone, for its roofline: the search less the same
+    # selection run from the same masses (scores given)
+    tsel = Timer()
+    for i in range(1 + max(3, args.steps)):
+        tsel("sel" if i else "warm", ad.block_search, None, None, None, block=blk,
+             text_start=w.text_start, text_len=w.text_len, mode="coverage", head_param_bp=tau,
+             scores=res.block_mass, shape=(B, H, L, D), workspace=ws)
+    sel_ms = float(np.mean(tsel.collect()["sel"]))
+    mass_ms = search_ms - sel_ms
+    n_scores = float(B * H * L * L)
+    mass_peak = VALU_LANE_OPS_PER_S / MASS_SLOTS_PER_SCORE / 1e12
+    roof_mass = {"kernel": "block_mass (search less its selection)", "bound": "alu",
+                 "achieved": round(n_scores / (mass_ms * 1e-3) / 1e12, 3), "peak": round(mass_peak, 3),
+                 "unit": "Tscore/s", "frac": round(n_scores / (mass_ms * 1e-3) / 1e12 / mass_peak, 4),
+                 "mass_ms": round(mass_ms, 3), "selection_ms": round(sel_ms, 3),
+                 "mfma_tflops": round(tf(f_mass, mass_ms), 1),
+                 "mfma_frac": round(tf(f_mass, mass_ms) / PEAK_BF16_TFLOPS, 4)}
     detail = {"head_k": head_k.tolist(), "head_recall_min": float(head_rec.min()),
               "head_recall_mean": float(head_rec.mean())}
 
@@ -770,7 +794,8 @@ def main():
         "fused_online_search": fused,
         "amortised_loop": amort,
         "two_phase_schedule": two_phase, "detail": detail,
-        "roofline": roof, "roofline_sparse_keep20": roof_sparse, "cpu_baseline": cpu,
+        "roofline": roof, "roofline_sparse_keep20": roof_sparse, "roofline_block_mass": roof_mass,
+        "cpu_baseline": cpu,
     }
     print(json.dumps(line), flush=True)
 
