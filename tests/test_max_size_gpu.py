@@ -1,14 +1,16 @@
 """GPU parity at the largest problems the library accepts, against the oracle
 on sampled rows.
 
-- Block-sparse attention (Sec. 4.1) at the largest head: L * D just under
-  2^30 elements, so a head's K and V reach 2^31 bytes less 27 KB and every
-  in-kernel byte offset sits near the top of its 32-bit range.  Rows keep the
-  text blocks, their own block, one block spread over the whole sequence and
-  the ragged last block (20 rows).
-- Dense attention + LSE, the block masses and the selection (Sec. 2.2, 4.1,
-  4.3) at the most key blocks a search takes (8,192 at block 128, L just
-  over one million tokens, the last block ragged).
+- Block-sparse attention (Sec. 4.1) at the largest head, d = 64 and 128:
+  L * D just under 2^30 elements, so a head's K and V each come within 28 KB
+  of 2^31 bytes and every in-kernel byte offset sits near the top of its
+  32-bit range.  Rows keep the text blocks, their own block, one block spread
+  over the whole sequence and the ragged last block.
+- Dense attention + LSE, the block masses, the selection and block-sparse
+  attention on the selected pattern (Sec. 2.2, 4.1, 4.3) at the most key
+  blocks a search takes (8,192), at block 128 (L just over one million
+  tokens) and block 64 (the block-64 kernel's map of one row's key blocks is
+  then full), the last block ragged.
 """
 import numpy as np
 import pytest
@@ -21,14 +23,20 @@ from _helpers import check_lse, check_mass, check_out, f64
 
 pytestmark = pytest.mark.gpu
 
-# 256 text tokens + 32 frames of 262,133 patches (the last frame 12 tokens
-# short): 65,536 blocks of 128, the last one 20 rows.
-MAX_HEAD = Workload("max_head_L8388500_H1_d128_b128", 1, 1, 128, 8388500, 256, 32, 262133, 128,
-                    seed=21)
-# 256 text tokens + 32 frames of 32,758 patches: 8,192 blocks of 128, the last
-# one 52 rows.
-MAX_BLOCKS = Workload("max_blocks_L1048500_H1_d128_b128", 1, 1, 128, 1048500, 256, 32, 32758, 128,
-                      seed=22)
+# 256 text tokens + 32 frames (the last one a few tokens short).  d = 128:
+# 65,536 blocks of 128, the last one 20 rows; d = 64: 131,071 blocks, the
+# last one 40 rows.
+MAX_HEAD = {
+    128: Workload("max_head_L8388500_H1_d128_b128", 1, 1, 128, 8388500, 256, 32, 262133, 128, seed=21),
+    64: Workload("max_head_L16777000_H1_d64_b128", 1, 1, 64, 16777000, 256, 32, 524274, 128, seed=23),
+}
+# 8,192 key blocks: block 128 (256 text tokens + 32 frames of 32,758 patches,
+# the last block 52 rows) and block 64 (32 frames of 16,375 patches, the last
+# block 26 rows).
+MAX_BLOCKS = {
+    128: Workload("max_blocks_L1048500_H1_d128_b128", 1, 1, 128, 1048500, 256, 32, 32758, 128, seed=22),
+    64: Workload("max_blocks_L524250_H1_d128_b64", 1, 1, 128, 524250, 256, 32, 16375, 64, seed=24),
+}
 
 
 def _rows(p, block, L):
@@ -56,12 +64,13 @@ def _spread_pattern(nb, n_text):
     return row_ptr.astype(np.int32), cand[keep].astype(np.int32)
 
 
-def test_sparse_at_largest_head():
-    w = MAX_HEAD
+@pytest.mark.parametrize("D", [128, 64])
+def test_sparse_at_largest_head(D):
+    w = MAX_HEAD[D]
     L, blk = w.seqlen, w.block
-    assert L * w.head_dim < 2 ** 30 and L * w.head_dim * 2 > 2 ** 31 - 32768
+    assert L * D < 2 ** 30 and L * D * 2 > 2 ** 31 - 28 * 1024
     nb = w.nblocks
-    assert nb == 65536 and L - (nb - 1) * blk == 20
+    assert (nb, L - (nb - 1) * blk) == ({128: (65536, 20), 64: (131071, 40)}[D])
     print(f"[max] {w.name}: inputs", flush=True)
     q, k, v = make_qkv(w, device="cuda")
     tb = text_blocks(L, blk, w.text_start, w.text_len)
@@ -83,11 +92,12 @@ def test_sparse_at_largest_head():
         check_lse(lse[0, 0, qi], l_ref, f"query block {p}")
 
 
-def test_dense_mass_and_selection_at_most_blocks():
-    w = MAX_BLOCKS
+@pytest.mark.parametrize("block", [128, 64])
+def test_dense_search_sparse_at_most_blocks(block):
+    w = MAX_BLOCKS[block]
     L, blk = w.seqlen, w.block
     nb = w.nblocks
-    assert nb == 8192 and L - (nb - 1) * blk == 52
+    assert nb == 8192 and L - (nb - 1) * blk == {128: 52, 64: 26}[block]
     print(f"[max] {w.name}: inputs", flush=True)
     q, k, v = make_qkv(w, device="cuda")
     print(f"[max] {w.name}: dense attention + LSE", flush=True)
@@ -99,6 +109,10 @@ def test_dense_mass_and_selection_at_most_blocks():
     tb = text_blocks(L, blk, w.text_start, w.text_len)
     kk = oracle.topk_count(50, nb, len(tb))
     assert kk == 41 and int(res.head_k[0, 0]) == kk
+    print(f"[max] {w.name}: block-sparse attention on the selected pattern", flush=True)
+    sp_out, sp_lse = ad.block_sparse_attn(q, k, v, res.row_ptr, res.col_idx, block=blk,
+                                          text_start=w.text_start, text_len=w.text_len)
+    torch.cuda.synchronize()
 
     # each row of masses from the fresh LSE sums to the row's query count
     sums = res.block_mass[0, 0].double().sum(-1).cpu().numpy()
@@ -106,10 +120,13 @@ def test_dense_mass_and_selection_at_most_blocks():
     expect[-1] = L - (nb - 1) * blk
     np.testing.assert_allclose(sums, expect, rtol=1e-3)
 
-    # dense output, LSE and masses of sampled query blocks against the oracle
+    # dense output, LSE and masses of sampled query blocks against the oracle,
+    # and block-sparse attention of those blocks over the keys they keep
     print(f"[max] {w.name}: oracle on sampled query blocks", flush=True)
     kh, vh = f64(k[0, 0]), f64(v[0, 0])
-    for p in (0, 2, 4000, nb - 2, nb - 1):
+    rpn = res.row_ptr.cpu().numpy().astype(np.int64)
+    ci = res.col_idx[: int(rpn[-1])].cpu().numpy()
+    for p in (0, len(tb), len(tb) + 1, 4000, 4001, nb - 2, nb - 1):
         qr = _rows(p, blk, L)
         qi = torch.as_tensor(qr, device="cuda")
         qh = f64(q[0, 0, qi])
@@ -118,13 +135,15 @@ def test_dense_mass_and_selection_at_most_blocks():
         check_lse(lse[0, 0, qi], l_ref, f"dense, query block {p}")
         m_ref = oracle.block_mass_rows(qh, kh, l_ref, w.scale, blk)
         check_mass(res.block_mass[0, 0, p], m_ref, f"masses, query block {p}")
+        kr = _key_rows(ci[rpn[p]:rpn[p + 1]], blk, L)
+        o_ref, l_ref = oracle.masked_attention(qh, kh[kr], vh[kr], np.ones(len(kr), bool), w.scale)
+        check_out(sp_out[0, 0, qi], o_ref, f"sparse, query block {p}")
+        check_lse(sp_lse[0, 0, qi], l_ref, f"sparse, query block {p}")
     del kh, vh
 
     # selection from the GPU's own masses: bit-exact on sampled rows (TOPK
     # rows are independent given the count)
-    rpn = res.row_ptr.cpu().numpy().astype(np.int64)
     assert rpn[0] == 0 and np.all(np.diff(rpn) == np.where(np.isin(np.arange(nb), tb), nb, kk))
-    ci = res.col_idx[: int(rpn[-1])].cpu().numpy()
     rng = np.random.default_rng(5)
     sample = sorted(set(tb) | {2, nb - 2, nb - 1} | set(rng.choice(nb, 40, replace=False).tolist()))
     for p in sample:
