@@ -235,3 +235,34 @@ def test_hierarchical_selection_bit_exact(case, base_bp, thr_bp):
     sel = oracle.select_blocks(W.numpy(), L, block, ts, tl, "hierarchical", [0] * H,
                                base_sparsity_bp=base_bp, recall_threshold_bp=thr_bp)
     _compare_selection(res, sel)
+
+
+@pytest.mark.parametrize("D,block,L,ts", [(64, 64, 1000, 0), (128, 128, 1000, 1), (128, 64, 777, 0),
+                                          (64, 128, 4096, 5)])
+@pytest.mark.parametrize("mode", ["topk", "coverage", "hierarchical"])
+def test_all_text_sequence_keeps_every_block(D, block, L, ts, mode):
+    """Degenerate text sink (Sec. 4.3): when the text overlaps every key block
+    (text from token ts to the end, ts inside block 0), every query block is
+    a text row and keeps every key block in every mode, and block-sparse
+    attention on that pattern equals dense attention bit for bit (the sparse
+    kernels then take the rows in plain order)."""
+    w = TINY.replace(head_dim=D, block=block, seqlen=L, text_len=L - ts, patches=2,
+                     text_first=(ts == 0))
+    assert w.text_start == ts
+    q, k, v = make_qkv(w, device="cuda")
+    B, H, nb = w.batch, w.heads, w.nblocks
+    od, ld = ad.dense_attn_lse(q, k, v)
+    params = [0] * H if mode == "hierarchical" else [9000 if mode == "coverage" else 100] * H
+    res = ad.block_search(q, k, ld, block=block, text_start=ts, text_len=w.text_len, mode=mode,
+                          head_param_bp=None if mode == "hierarchical" else params,
+                          base_sparsity_bp=9000)
+    os_, ls = ad.block_sparse_attn(q, k, v, res.row_ptr, res.col_idx, block=block, text_start=ts,
+                                   text_len=w.text_len)
+    torch.cuda.synchronize()
+    rp, ci = csr_rows(res.row_ptr, res.col_idx)
+    assert np.array_equal(rp, np.arange(B * H * nb + 1) * nb)
+    assert np.array_equal(ci, np.tile(np.arange(nb), B * H * nb))
+    assert torch.equal(od, os_) and torch.equal(ld, ls)
+    sel = oracle.select_blocks(res.block_mass.cpu().numpy(), L, block, ts, w.text_len, mode, params,
+                               base_sparsity_bp=9000)
+    _compare_selection(res, sel)
