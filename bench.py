@@ -668,7 +668,8 @@ def main():
                  "unit": "Tscore/s", "frac": round(n_scores / (mass_ms * 1e-3) / 1e12 / mass_peak, 4),
                  "mass_ms": round(mass_ms, 3), "selection_ms": round(sel_ms, 3),
                  "mfma_tflops": round(tf(f_mass, mass_ms), 1),
-                 "mfma_frac": round(tf(f_mass, mass_ms) / PEAK_BF16_TFLOPS, 4)}
+                 "mfma_frac": round(tf(f_mass, mass_ms) / PEAK_BF16_TFLOPS, 4),
+                 "traffic": measured_traffic("mass")}
     detail = {"head_k": head_k.tolist(), "head_recall_min": float(head_rec.min()),
               "head_recall_mean": float(head_rec.mean())}
 
