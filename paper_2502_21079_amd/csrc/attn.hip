@@ -885,11 +885,11 @@ __global__ __launch_bounds__(64 * NW, NW >= 8 ? 1 : 2) void attn_sparse_pair_ker
 // adjacent query blocks (two of 128 or four of 64), so every K tile brought
 // into LDS serves 256 rows, and two workgroups share a CU (four waves per
 // SIMD: the pass needs under 128 registers).  Against workgroups of 128 rows
-// this halves the tile traffic per FLOP; the pass is exp-bound, and on this
-// power-limited chip the saving shows as clock (110K: 67.1 -> 65.1 ms at
-// block 128, 70.3 -> 68.9 ms at block 64, masses bitwise unchanged).  Full
-// key tiles run through a
-// software pipeline: step t forms the scores of tile t+1 (QK MFMAs) while the
+// this halves the tile traffic per FLOP; the pass is bound by its QK MFMAs
+// at the clock the chip's power allows (the exponentials hide under the
+// other waves' MFMAs), so the saving shows as clock (110K: 67.1 -> 65.1 ms
+// at block 128, 70.3 -> 68.9 ms at block 64, masses bitwise unchanged).
+// Full key tiles run through a software pipeline: step t forms the scores of tile t+1 (QK MFMAs) while the
 // VALU exponentiates and sums tile t; K is double-buffered and the loads of
 // tile t+2 are spread over the step.  Per-wave sums of a finished key block
 // are combined in a fixed order into an LDS ring per query block, which is
@@ -990,8 +990,8 @@ __device__ __forceinline__ void block_mass_body(const MassParams& a, int bh, int
       asm volatile("" : "+s"(fill));
       auto loads = [&](int slot) {
         // Load n goes to slot n * NM / NTOT: spread over the whole step here
-        // (front-loaded as in attn_fwd_kernel this exp-heavy pass ran 3-5%
-        // slower).
+        // (front-loaded as in attn_fwd_kernel this pass, with twice the
+        // VALU work per MFMA, ran 3-5% slower).
         constexpr int NTOT = KLoader<D, NW>::PW, NM = 2 * NK;
         static_assert(NTOT <= NM, "one load instruction per slot at most");
         const int n = (slot * NTOT + NM - 1) / NM;
