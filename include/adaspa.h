@@ -17,7 +17,9 @@
  *                             key blocks (Sec. 4.1, bias form with c -> inf)
  *
  * and adaspa_fused_online_search, the first two in one launch as Algorithm 1
- * describes them (dense attention + LSE, then the masses of the same rows).
+ * describes them (dense attention + LSE, then the masses of the same rows),
+ * and adaspa_single_pass_online_search, the same results with one pass over
+ * Q K^T instead of two.
  *
  * Conventions shared by every call
  * --------------------------------
@@ -203,6 +205,47 @@ adaspa_status adaspa_fused_online_search(const adaspa_problem* prob, const void*
                                          int32_t* head_k, float* head_recall,
                                          void* workspace, size_t workspace_bytes,
                                          void* stream);
+
+/* Device bytes of the workspace of adaspa_single_pass_online_search: the
+ * workspace of adaspa_block_search plus B*H*NB*L floats of per-row block
+ * masses (NB = ceil(L/Bs); 9.1 GB for B=1, H=24, L=110,336, Bs=128), rounded
+ * up to 256 bytes.  0 for invalid arguments or ADASPA_F_SCORES_GIVEN. */
+size_t adaspa_single_pass_online_search_workspace(const adaspa_problem* prob,
+                                                  const adaspa_select* sel);
+
+/* Single-pass online search (Algorithm 1, Sec. 4.1-4.2, with one pass over
+ * Q K^T): the outputs of adaspa_fused_online_search, computed differently.
+ * The block mass W[p][c] is the sum over rows i of p of exp(s_ij - LSE_i)
+ * over the keys j of c.  The attention pass already forms
+ * exp(s_ij - m_i) for its softmax (m_i the row's running reference), so it
+ * also adds those terms per (row, key block) in fp32 and keeps
+ * log2 of each sum plus m_i in the workspace; once a row's LSE is known the
+ * kernel turns them into the row's shares exp(y - LSE_i) and sums them over
+ * the rows of each query block.  The second recomputation of Q K^T that the
+ * two-pass form needs is not taken.
+ *   out, lse          bit for bit those of adaspa_dense_attn_lse (lse may be
+ *                     NULL: the masses still use the fresh LSE)
+ *   block_mass        the masses of the fresh LSE, equal to those of
+ *                     adaspa_block_search up to fp32 rounding (a different
+ *                     order of the same sums), within 1e-3 relative of the
+ *                     exact values
+ *   row_ptr, col_idx, head_k, head_recall
+ *                     the selection of those masses, as adaspa_block_search
+ *                     (ADASPA_F_SCORES_GIVEN is not allowed:
+ *                     ADASPA_ERR_INVALID_ARG)
+ * workspace must hold adaspa_single_pass_online_search_workspace() bytes,
+ * 256-byte aligned (ADASPA_ERR_WORKSPACE otherwise); it holds the
+ * selection's scratch, the per-XCD work-queue counters (cleared by the call)
+ * and the per-row block masses, and its contents need not be kept between
+ * calls.  Capacity, alignment and the other errors as adaspa_block_search. */
+adaspa_status adaspa_single_pass_online_search(const adaspa_problem* prob, const void* q,
+                                               const void* k, const void* v, void* out,
+                                               float* lse, const adaspa_select* sel,
+                                               float* block_mass, int32_t* row_ptr,
+                                               int32_t* col_idx, int64_t col_capacity,
+                                               int32_t* head_k, float* head_recall,
+                                               void* workspace, size_t workspace_bytes,
+                                               void* stream);
 
 /* Device bytes of the optional workspace of adaspa_block_sparse_attn (0 for
  * invalid arguments). */

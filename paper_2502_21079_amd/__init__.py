@@ -28,7 +28,8 @@ import torch
 __all__ = ["dense_attn_lse", "dense_attn_workspace", "block_search", "block_sparse_attn",
            "block_sparse_attn_workspace", "block_sparse_attn_noalloc", "SearchResult",
            "library_path", "load_library", "AdaspaError", "EXPORTED_SYMBOLS",
-           "block_search_workspace", "block_search_capacity", "fused_online_search"]
+           "block_search_workspace", "block_search_capacity", "fused_online_search",
+           "single_pass_online_search", "single_pass_online_search_workspace"]
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
 _LIB_NAME = "libadaspa.so"
@@ -37,7 +38,8 @@ EXPORTED_SYMBOLS = ("adaspa_status_string", "adaspa_dense_attn_workspace", "adas
                     "adaspa_block_search_workspace", "adaspa_block_search_capacity",
                     "adaspa_block_search", "adaspa_block_sparse_attn_workspace",
                     "adaspa_block_sparse_attn", "adaspa_block_sparse_attn_noalloc",
-                    "adaspa_fused_online_search")
+                    "adaspa_fused_online_search", "adaspa_single_pass_online_search_workspace",
+                    "adaspa_single_pass_online_search")
 
 SELECT_TOPK = 0
 SELECT_COVERAGE = 1
@@ -98,6 +100,11 @@ def load_library():
     lib.adaspa_fused_online_search.restype = ctypes.c_int
     lib.adaspa_fused_online_search.argtypes = [P, vp, vp, vp, vp, f32p, S, f32p, i32p, i32p,
                                                ctypes.c_int64, i32p, f32p, vp, ctypes.c_size_t, vp]
+    lib.adaspa_single_pass_online_search_workspace.restype = ctypes.c_size_t
+    lib.adaspa_single_pass_online_search_workspace.argtypes = [P, S]
+    lib.adaspa_single_pass_online_search.restype = ctypes.c_int
+    lib.adaspa_single_pass_online_search.argtypes = [P, vp, vp, vp, vp, f32p, S, f32p, i32p, i32p,
+                                                     ctypes.c_int64, i32p, f32p, vp, ctypes.c_size_t, vp]
     lib.adaspa_block_sparse_attn_workspace.restype = ctypes.c_size_t
     lib.adaspa_block_sparse_attn_workspace.argtypes = [P]
     lib.adaspa_block_sparse_attn.restype = ctypes.c_int
@@ -351,6 +358,64 @@ def fused_online_search(q, k, v, *, block: int, text_start: int, text_len: int, 
                                           int(res.col_idx.numel()), _ptr(res.head_k),
                                           _ptr(res.head_recall), _ptr(workspace),
                                           int(workspace.numel()), _stream(dev)))
+    return out, lse, res
+
+
+def single_pass_online_search_workspace(shape, block, text_start, text_len, mode, head_param_bp=None,
+                                        text_sink=True, base_sparsity_bp: int = 8000,
+                                        recall_threshold_bp: int = 8000) -> int:
+    """Bytes of the workspace of :func:`single_pass_online_search`: the
+    search's scratch plus B*H*NB*L floats of per-row block masses."""
+    B, H, L, D = shape
+    prob = _problem_shape(B, H, L, D, block, text_start, text_len, None)
+    sel, _keep = _select(mode, head_param_bp, text_sink, False, base_sparsity_bp, recall_threshold_bp,
+                         heads=H)
+    return int(load_library().adaspa_single_pass_online_search_workspace(ctypes.byref(prob),
+                                                                         ctypes.byref(sel)))
+
+
+def single_pass_online_search(q, k, v, *, block: int, text_start: int, text_len: int, mode: str,
+                              head_param_bp: Optional[Sequence[int]] = None, text_sink: bool = True,
+                              scale: Optional[float] = None, out=None, lse=None, want_lse: bool = True,
+                              workspace: Optional[torch.Tensor] = None, base_sparsity_bp: int = 8000,
+                              recall_threshold_bp: int = 8000,
+                              result: Optional["SearchResult"] = None):
+    """Algorithm 1 with one pass over Q K^T: dense attention with its LSE, the
+    block masses of that LSE (added per key block from the attention pass's
+    own exponentials) and the selection.  Returns (out, lse, SearchResult):
+    out and lse bit for bit those of :func:`dense_attn_lse`, the masses those
+    of :func:`block_search` up to fp32 rounding.  ``workspace`` (uint8 CUDA
+    tensor of at least :func:`single_pass_online_search_workspace` bytes) is
+    allocated here when not given."""
+    _check_qkv(q, k, v)
+    lib = load_library()
+    B, H, L, D = q.shape
+    dev = q.device
+    nb = (L + block - 1) // block
+    prob = _problem_shape(B, H, L, D, block, text_start, text_len, scale)
+    sel, _keep = _select(mode, head_param_bp, text_sink, False, base_sparsity_bp,
+                         recall_threshold_bp, heads=H)
+    cap = lib.adaspa_block_search_capacity(ctypes.byref(prob), ctypes.byref(sel))
+    wsb = lib.adaspa_single_pass_online_search_workspace(ctypes.byref(prob), ctypes.byref(sel))
+    if cap < 0 or wsb == 0:
+        _check(lib.adaspa_single_pass_online_search(ctypes.byref(prob), None, None, None, None, None,
+                                                    ctypes.byref(sel), None, None, None, 0, None, None,
+                                                    None, 0, None))
+        raise AdaspaError("invalid single_pass_online_search arguments")
+    _check_outputs(q, out, lse)
+    if out is None:
+        out = torch.empty_like(q)
+    if lse is None and want_lse:
+        lse = torch.empty(B, H, L, dtype=torch.float32, device=dev)
+    res = _search_outputs(B, H, nb, cap, dev, result)
+    if workspace is None or workspace.numel() < wsb:
+        workspace = torch.empty(int(wsb), dtype=torch.uint8, device=dev)
+    _check(lib.adaspa_single_pass_online_search(ctypes.byref(prob), _ptr(q), _ptr(k), _ptr(v), _ptr(out),
+                                                _ptr(lse), ctypes.byref(sel), _ptr(res.block_mass),
+                                                _ptr(res.row_ptr), _ptr(res.col_idx),
+                                                int(res.col_idx.numel()), _ptr(res.head_k),
+                                                _ptr(res.head_recall), _ptr(workspace),
+                                                int(workspace.numel()), _stream(dev)))
     return out, lse, res
 
 

@@ -375,6 +375,59 @@ adaspa_status adaspa_fused_online_search(const adaspa_problem* prob, const void*
   return enqueue_selection(prob, sel, block_mass, row_ptr, col_idx, head_k, head_recall, workspace, s);
 }
 
+size_t adaspa_single_pass_online_search_workspace(const adaspa_problem* prob, const adaspa_select* sel) {
+  if (check_problem(prob) != ADASPA_OK || check_select(prob, sel) != ADASPA_OK) return 0;
+  if (sel->flags & ADASPA_F_SCORES_GIVEN) return 0;
+  const size_t bh = (size_t)prob->batch * prob->heads;
+  return workspace_layout(prob).total + align_up(bh * (size_t)num_blocks(prob) * prob->seqlen * sizeof(float)) +
+         align_up(bh * (size_t)prob->seqlen * sizeof(float));
+}
+
+adaspa_status adaspa_single_pass_online_search(const adaspa_problem* prob, const void* q, const void* k,
+                                               const void* v, void* out, float* lse,
+                                               const adaspa_select* sel, float* block_mass,
+                                               int32_t* row_ptr, int32_t* col_idx, int64_t col_capacity,
+                                               int32_t* head_k, float* head_recall, void* workspace,
+                                               size_t workspace_bytes, void* stream) {
+  adaspa_status st = check_problem(prob);
+  if (st != ADASPA_OK) return st;
+  st = check_select(prob, sel);
+  if (st != ADASPA_OK) return st;
+  if (sel->flags & ADASPA_F_SCORES_GIVEN) return ADASPA_ERR_INVALID_ARG;
+  if (!q || !k || !v || !out || !block_mass || !row_ptr || !col_idx) return ADASPA_ERR_INVALID_ARG;
+  if (!aligned16(q) || !aligned16(k) || !aligned16(v) || !aligned16(out) ||
+      (lse && ((uintptr_t)lse & 3u)) || ((uintptr_t)block_mass & 3u) ||
+      ((uintptr_t)row_ptr & 3u) || ((uintptr_t)col_idx & 3u))
+    return ADASPA_ERR_INVALID_ARG;
+  const int64_t need = adaspa_block_search_capacity(prob, sel);
+  if (col_capacity < need) return ADASPA_ERR_CAPACITY;
+  const WsLayout wl = workspace_layout(prob);
+  if (!workspace || workspace_bytes < adaspa_single_pass_online_search_workspace(prob, sel) ||
+      ((uintptr_t)workspace % kAlign))
+    return ADASPA_ERR_WORKSPACE;
+
+  hipStream_t s = (hipStream_t)stream;
+  AttnParams a;
+  memset(&a, 0, sizeof a);
+  a.q = (const u16*)q;
+  a.k = (const u16*)k;
+  a.v = (const u16*)v;
+  a.o = (u16*)out;
+  a.lse = lse;
+  a.batch_heads = prob->batch * prob->heads;
+  a.seqlen = prob->seqlen;
+  a.block = prob->block;
+  a.nkb = num_blocks(prob);
+  a.scale = scale_of(prob);
+  a.scale_log2 = a.scale * 1.4426950408889634f;
+  a.claim = (uint32_t*)((char*)workspace + wl.claim);
+  a.ylog = (float*)((char*)workspace + wl.total);
+  a.ylse2 = (float*)((char*)workspace + wl.total +
+                     align_up((size_t)a.batch_heads * a.nkb * prob->seqlen * sizeof(float)));
+  a.wmass = block_mass;
+  if (launch_single_pass_search(a, prob->head_dim, s) != hipSuccess) return ADASPA_ERR_HIP;
+  return enqueue_selection(prob, sel, block_mass, row_ptr, col_idx, head_k, head_recall, workspace, s);
+}
 
 adaspa_status adaspa_block_sparse_attn(const adaspa_problem* prob, const void* q, const void* k,
                                        const void* v, const int32_t* row_ptr,

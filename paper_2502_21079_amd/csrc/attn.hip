@@ -65,8 +65,13 @@ struct NoTail {
   __device__ __forceinline__ void operator()(T&&...) const {}
 };
 
-template <int D, int NW, bool SPARSE, typename Tail>
+// With BS (dense only) the body also writes, for every row and key block c,
+// log2 of the row's unnormalised mass in block c plus the row's reference at
+// that time, so that the block's share of the row's softmax is
+// exp2(ylog - LSE * log2(e)) (the single-pass search below).
+template <int D, int NW, bool SPARSE, bool BS = false, typename Tail>
 __device__ __forceinline__ void attn_fwd_body(AttnParams a, Tail&& tail) {
+  static_assert(!(SPARSE && BS), "block masses come from the dense pass");
   constexpr int NT = 64 * NW;
   using KDMA = TileDMA<D, NW, 1>;
   using VDMA = TileDMA<D, NW, 2>;
@@ -212,6 +217,28 @@ __device__ __forceinline__ void attn_fwd_body(AttnParams a, Tail&& tail) {
   const float sl2 = a.scale_log2;
   RowRef ref;                             // softmax reference of this lane's row
   float lsum = 0.f;                       // this lane's half of the row sum
+  // BS: this lane's fp32 sum of exp2(s * sl2 - ref.mc) over the current key
+  // block so far; written out (both halves of the row added) when the block
+  // ends, as log2 of the sum plus ref.mc.  rowf is the same sum over the whole
+  // row: the masses are normalised by it rather than by the sum of the
+  // bf16-rounded weights behind the output and its LSE, whose rounding (up
+  // to 2^-9 of a weight) would shift every mass of a row dominated by a few
+  // keys by as much.
+  float bsum = 0.f, rowf = 0.f;
+  const int tsh = (BS && a.block == 128) ? 1 : 0;   // log2 of the tiles per key block
+  const int tpb = 1 << tsh;
+  auto flush_block = [&](int c) {
+    if constexpr (BS) {
+      float lo, hi;
+      half_pair(bsum, lo, hi);
+      const float b = lo + hi;
+      // Column c of this head's [nkb, L] slab: a wave-uniform base, and the
+      // row as a 32-bit offset.
+      float* col = a.ylog + ((size_t)bh * a.nkb + (size_t)__builtin_amdgcn_readfirstlane(c)) * (size_t)L;
+      if (hw == 0 && qrow < L) col[qrow] = (b > 0.f ? __builtin_amdgcn_logf(b) : -INFINITY) + ref.mc;
+      bsum = 0.f;
+    }
+  };
   f32x16 o[ND];
 #pragma unroll
   for (int d = 0; d < ND; ++d) o[d] = f32x16{};
@@ -305,9 +332,19 @@ __device__ __forceinline__ void attn_fwd_body(AttnParams a, Tail&& tail) {
       };
       f32x16 s_next[2];
       bf16x8 p_cur[2][2];
-      pipelined_step<D, KS, VS>(loads, rdK + klane, rdV + voff, qf, s_cur, p_prev, s_next, p_cur, o, sl2,
-                                ref.mc, rsum);
-      move_reference(ref, rsum, bad, s_cur, p_cur, pend, pend_alpha, sl2, c32);
+      float tsum = 0.f;
+      pipelined_step<D, KS, VS, 2, BS>(loads, rdK + klane, rdV + voff, qf, s_cur, p_prev, s_next, p_cur, o,
+                                       sl2, ref.mc, rsum, &tsum);
+      move_reference<2, BS>(ref, rsum, bad, s_cur, p_cur, pend, pend_alpha, sl2, c32, false, &tsum);
+      if constexpr (BS) {
+        if (pend) {                     // the reference moved at this tile
+          bsum *= pend_alpha;
+          rowf *= pend_alpha;
+        }
+        bsum += tsum;
+        rowf += tsum;
+        if (((t + 1) & (tpb - 1)) == 0) flush_block(t >> tsh);
+      }
 #pragma unroll
       for (int g = 0; g < 2; ++g) {
         s_cur[g] = s_next[g];
@@ -342,6 +379,8 @@ __device__ __forceinline__ void attn_fwd_body(AttnParams a, Tail&& tail) {
   if (redo) {
     ref = RowRef{};
     lsum = 0.f;
+    bsum = 0.f;
+    rowf = 0.f;
 #pragma unroll
     for (int d = 0; d < ND; ++d) o[d] = f32x16{};
   }
@@ -359,7 +398,15 @@ __device__ __forceinline__ void attn_fwd_body(AttnParams a, Tail&& tail) {
       qk_tile<D, KS>(sK[0], qf, c32, hw, s);
       mask_tile(s, L - kb, hw);
       bf16x8 pb[2][2];
-      const float alpha = softmax_tile(s, ref, lsum, sl2, pb);
+      float alpha;
+      if constexpr (BS) {
+        float fs;
+        alpha = softmax_tile_fsum(s, ref, lsum, sl2, pb, fs);
+        bsum = bsum * alpha + fs;
+        rowf = rowf * alpha + fs;
+      } else {
+        alpha = softmax_tile(s, ref, lsum, sl2, pb);
+      }
 #pragma unroll
       for (int d = 0; d < ND; ++d)
 #pragma unroll
@@ -389,8 +436,14 @@ __device__ __forceinline__ void attn_fwd_body(AttnParams a, Tail&& tail) {
     if (nf == 0 && spec >= 0) wait_vmem();    // no guessed load is left in flight
   } else {
     if (any_redo)
-      for (int t = 0; t < nf; ++t) masked_tile(t * KT, redo);
+      for (int t = 0; t < nf; ++t) {
+        masked_tile(t * KT, redo);
+        if (redo && ((t + 1) & (tpb - 1)) == 0) flush_block(t >> tsh);
+      }
     if (nf * KT < L) masked_tile(nf * KT, true);
+    // The last key block: the ragged tile, or full tiles that stopped short
+    // of a whole block.
+    if (nf * KT < L || (nf & (tpb - 1)) != 0) flush_block(nf >> tsh);
   }
 
   // Normalise and store.
@@ -409,7 +462,15 @@ __device__ __forceinline__ void attn_fwd_body(AttnParams a, Tail&& tail) {
     a.lse[(size_t)bh * L + qrow] = lt > 0.f ? fmaf(ref.m, a.scale, logf(lt)) : -INFINITY;
   // The row's Q fragments, its sum and reference (LSE = m * scale + log lt)
   // and the K/V ring, which no wave reads any more after the next barrier.
-  tail(bh, qt, qf, lt, ref.m, &sKV[0][0]);
+  // With BS: the unrounded row sum and the reference in log2 units instead
+  // (log2 e * LSE = mc + log2 of that sum, up to fp32 rounding).
+  if constexpr (BS) {
+    float lo, hi;
+    half_pair(rowf, lo, hi);
+    tail(bh, qt, qf, lo + hi, ref.mc, &sKV[0][0]);
+  } else {
+    tail(bh, qt, qf, lt, ref.m, &sKV[0][0]);
+  }
 }
 
 template <int D, int NW, bool SPARSE>
@@ -1119,6 +1180,68 @@ __global__ __launch_bounds__(512, 1) void fused_search_kernel(AttnParams a, Mass
 }
 
 // ---------------------------------------------------------------------------
+// Single-pass online search (Algorithm 1 with one pass over Q K^T).  The mass
+// of block (p, c) is the sum over rows i of p and keys j of c of
+// exp(s_ij - LSE_i).  With the row's reference m_i (raw score units) that is
+// the sum over i of exp2(ylog_ic - LSE_i log2 e), where ylog_ic = log2(sum_j
+// exp2((s_ij - m_i) scale log2 e)) + m_i scale log2 e.  The attention pass
+// takes every exp2((s_ij - m_i) scale log2 e) for its softmax anyway, so it
+// adds their fp32 values per key block and writes ylog (attn_fwd_body with
+// BS), and at the end of each row log2 e * LSE_i.  That LSE is the one of
+// the unrounded fp32 row sum (the stored LSE normalises the bf16-rounded
+// weights of the output), so each row's masses add up to one to fp32
+// rounding.  A second kernel then streams ylog once and sums the rows'
+// shares per block.  No second Q K^T is taken (the two-pass search
+// recomputes it in full).
+// ---------------------------------------------------------------------------
+template <int D>
+__global__ __launch_bounds__(512, 1) void single_pass_search_kernel(AttnParams a) {
+  constexpr int NW = 8;
+  attn_fwd_body<D, NW, false, true>(a, [&](int bh, int qt, const bf16x8 (&)[D / 16], float rowf, float mc,
+                                           u16*) {
+    const int lane = threadIdx.x & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    const int qrow = qt * (32 * NW) + wave * 32 + (lane & 31);
+    // A row without weight adds nothing to any block.
+    if (lane < 32 && qrow < a.seqlen)
+      a.ylse2[(size_t)bh * a.seqlen + qrow] = rowf > 0.f ? mc + __builtin_amdgcn_logf(rowf) : INFINITY;
+  });
+}
+
+// W[bh][p][c] = sum over the rows i of query block p of
+// exp2(ylog[bh][c][i] - ylse2[bh][i]).  One workgroup per (query block, head);
+// each wave takes groups of 64 key blocks, reads each block's rows of p with
+// one lane per row (whole 256-byte runs), sums them over the wave in a fixed
+// order, and stores the group's 64 masses together.
+__global__ __launch_bounds__(256) void single_pass_reduce_kernel(AttnParams a) {
+  const int p = blockIdx.x, bh = blockIdx.y;
+  const int L = a.seqlen, nkb = a.nkb;
+  const int lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int r0 = p * a.block;
+  const int nr = L - r0 < a.block ? L - r0 : a.block;     // rows of this query block
+  const bool v0 = lane < nr, v1 = lane + 64 < nr;         // this lane's rows r0 + lane, r0 + lane + 64
+  const float* l2 = a.ylse2 + (size_t)bh * L + r0;
+  const float m0 = v0 ? l2[lane] : 0.f, m1 = v1 ? l2[lane + 64] : 0.f;
+  const float* y = a.ylog + (size_t)bh * nkb * L + r0 + lane;
+  for (int cg = wave * 64; cg < nkb; cg += 4 * 64) {
+    const int n = nkb - cg < 64 ? nkb - cg : 64;
+    float w_mine = 0.f;                                   // lane j keeps block cg + j
+#pragma unroll 8
+    for (int j = 0; j < 64; ++j) {
+      if (j < n) {
+        const float* yc = y + (size_t)(cg + j) * L;
+        float s = v0 ? fast_exp2(yc[0] - m0) : 0.f;
+        if (v1) s += fast_exp2(yc[64] - m1);
+        const float w = wave_sum(s);
+        w_mine = lane == j ? w : w_mine;
+      }
+    }
+    if (lane < n) a.wmass[((size_t)bh * nkb + p) * nkb + cg + lane] = w_mine;
+  }
+}
+
+// ---------------------------------------------------------------------------
 // Launchers
 // ---------------------------------------------------------------------------
 template <int D, int NW, bool SPARSE>
@@ -1225,6 +1348,28 @@ hipError_t launch_fused_search(AttnParams a, MassParams m, int D, hipStream_t st
     if (D == 64) hipLaunchKernelGGL((fused_search_kernel<64, 2>), dim3(a.n_wg), dim3(512), 0, st, a, m);
     else hipLaunchKernelGGL((fused_search_kernel<128, 2>), dim3(a.n_wg), dim3(512), 0, st, a, m);
   }
+  return hipGetLastError();
+}
+
+hipError_t launch_single_pass_search(AttnParams a, int D, hipStream_t st) {
+  // Work items as in launch_dense: (head, 256-row query tile), two query
+  // blocks of 128 or four of 64.
+  a.row_ptr = nullptr;
+  a.col_idx = nullptr;
+  a.nqt = (a.seqlen + 255) / 256;
+  a.n_items = a.nqt * a.batch_heads;
+  a.n_wg = a.n_items;
+  if (a.claim != nullptr) {
+    a.n_wg = a.n_items + (a.n_items + 3) / 4;
+    hipLaunchKernelGGL(claim_reset_kernel, dim3(1), dim3(64), 0, st, a.claim);
+    const hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+  }
+  if (D == 64) hipLaunchKernelGGL((single_pass_search_kernel<64>), dim3(a.n_wg), dim3(512), 0, st, a);
+  else hipLaunchKernelGGL((single_pass_search_kernel<128>), dim3(a.n_wg), dim3(512), 0, st, a);
+  const hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(single_pass_reduce_kernel, dim3(a.nkb, a.batch_heads), dim3(256), 0, st, a);
   return hipGetLastError();
 }
 

@@ -446,6 +446,28 @@ __device__ __forceinline__ float exp_tile(const f32x16 (&s)[2], float sl2, float
   return ts;
 }
 
+// As exp_tile, and fsum also receives this lane's sum of the unrounded fp32
+// exponentials (for block masses, which must not carry the rounding of P).
+template <int G = 2>
+__device__ __forceinline__ float exp_tile_fsum(const f32x16 (&s)[2], float sl2, float mc, bf16x8 (&pb)[2][2],
+                                               float& fsum) {
+  const bf16x2 ones = {(__bf16)1.0f, (__bf16)1.0f};
+  float ts = 0.f, fs = 0.f;
+#pragma unroll
+  for (int g = 0; g < G; ++g)
+#pragma unroll
+    for (int e = 0; e < 16; e += 2) {
+      const float x0 = fast_exp2(fmaf(s[g][e], sl2, -mc)), x1 = fast_exp2(fmaf(s[g][e + 1], sl2, -mc));
+      const bf16x2 pr = {(__bf16)x0, (__bf16)x1};
+      pb[g][e >> 3][e & 7] = pr[0];
+      pb[g][e >> 3][(e & 7) + 1] = pr[1];
+      ts = __builtin_amdgcn_fdot2_f32_bf16(pr, ones, ts, false);
+      fs += x0 + x1;
+    }
+  fsum = fs;
+  return ts;
+}
+
 // End of a pipelined step (rare branch, taken by the whole wave): rows whose
 // running sum (tiles up to the previous one) passed kRowSumLimit move their
 // reference up by log2 of the sum, so the sum becomes about 1; rows without a
@@ -455,11 +477,12 @@ __device__ __forceinline__ float exp_tile(const f32x16 (&s)[2], float sl2, float
 // new reference.  bad is set when a sum has left the safe range.  A hidden
 // tile (block-64 pairs: one the other query block keeps) never sets the
 // reference and its probabilities stay exact zeros.
-template <int G = 2>
+// With BS, *tsum receives the fp32 sum of the retaken probabilities.
+template <int G = 2, bool BS = false>
 __device__ __forceinline__ void move_reference(RowRef& ref, RowSums& rsum, bool& bad,
                                                const f32x16 (&s_cur)[2], bf16x8 (&p_cur)[2][2],
                                                bool& pend, float& pend_alpha, float sl2, int c32,
-                                               bool hidden = false) {
+                                               bool hidden = false, float* tsum = nullptr) {
   const float sr = rsum.acc[0];
   if (!__any(ref.m == -INFINITY || sr > kRowSumLimit)) return;
   bad = bad || !(sr <= kRowSumBad);
@@ -477,7 +500,8 @@ __device__ __forceinline__ void move_reference(RowRef& ref, RowSums& rsum, bool&
   }
   pend_alpha = al;
   pend = true;
-  exp_tile<G>(s_cur, sl2, hidden ? INFINITY : ref.mc, p_cur);
+  if constexpr (BS) exp_tile_fsum<G>(s_cur, sl2, hidden ? INFINITY : ref.mc, p_cur, *tsum);
+  else exp_tile<G>(s_cur, sl2, hidden ? INFINITY : ref.mc, p_cur);
 }
 
 // After the last pipelined tile: its probabilities join the sums, a sum out
@@ -523,6 +547,21 @@ __device__ __forceinline__ float softmax_tile(const f32x16 (&s)[2], RowRef& ref,
     a = ref.raise(s, sl2);
     lsum *= a;
     ts = exp_tile(s, sl2, ref.mc, pb);
+  }
+  lsum += ts;
+  return a;
+}
+
+// As softmax_tile; fsum receives this lane's fp32 sum of the tile's
+// exponentials against the reference they were finally taken against.
+__device__ __forceinline__ float softmax_tile_fsum(const f32x16 (&s)[2], RowRef& ref, float& lsum, float sl2,
+                                                   bf16x8 (&pb)[2][2], float& fsum) {
+  float ts = exp_tile_fsum(s, sl2, ref.mc, pb, fsum);
+  float a = 1.f;
+  if (__any(ts > ref.lim)) {
+    a = ref.raise(s, sl2);
+    lsum *= a;
+    ts = exp_tile_fsum(s, sl2, ref.mc, pb, fsum);
   }
   lsum += ts;
   return a;
@@ -593,12 +632,14 @@ constexpr int kStageElems = NW * 32 * (D + 8);    // ring elements store_rows us
 // pipe and the VALU work side by side within the wave.  Four slots also add
 // the previous tile's rounded probabilities (the operands of its P V) to the
 // running row sums.
-template <int D, int KS, int VS, int G = 2, typename Hook>
+// With BS, *tsum receives this lane's sum of the current tile's unrounded
+// exponentials, added pair by pair as the pairs are rounded.
+template <int D, int KS, int VS, int G = 2, bool BS = false, typename Hook>
 __device__ __forceinline__ void pipelined_step(Hook&& hook, const u16* klane, const u16* vlane,
                                                const bf16x8 (&qf)[D / 16], const f32x16 (&s_cur)[2],
                                                const bf16x8 (&p_prev)[2][2], f32x16 (&s_next)[2],
                                                bf16x8 (&p_cur)[2][2], f32x16 (&o)[D / 32], float sl2,
-                                               float mc, RowSums& rsum) {
+                                               float mc, RowSums& rsum, float* tsum = nullptr) {
   constexpr int NK = D / 16, ND = D / 32;
   constexpr int NQK = G * NK, NPV = 2 * G * ND;      // G score groups of 32 keys
   static_assert(NQK == NPV, "QK and PV slots alternate");
@@ -643,6 +684,7 @@ __device__ __forceinline__ void pipelined_step(Hook&& hook, const u16* klane, co
   constexpr int PER = NS / NM;
   constexpr int RSP = NM / (2 * G);           // row-sum MFMAs in slots RSP/2 + j*RSP
   float arg[NS], ex[NS];
+  float fs = 0.f;
   auto stage_arg = [&](int i) {
 #pragma unroll
     for (int u = 0; u < PER; ++u) {
@@ -668,6 +710,10 @@ __device__ __forceinline__ void pipelined_step(Hook&& hook, const u16* klane, co
         pin(pr);
         p_cur[g][r >> 3][(r & 7) - 1] = pr[0];
         p_cur[g][r >> 3][r & 7] = pr[1];
+        if constexpr (BS) {
+          fs += ex[e - 1] + ex[e];
+          pin(fs);              // in this slot: deferred, the adds keep every exponential live
+        }
       }
     }
   };
@@ -688,6 +734,7 @@ __device__ __forceinline__ void pipelined_step(Hook&& hook, const u16* klane, co
   stage_exp(NM - 1);
   stage_sum(NM - 2);
   stage_sum(NM - 1);
+  if constexpr (BS) *tsum = fs;
 }
 
 // One pipelined step of the block-mass pass: the NM = 2*NK QK MFMAs of the

@@ -31,6 +31,12 @@ struct AttnParams {
   uint32_t* claim;            // 9 work-queue counters (one per XCD + a flag), or null
   int n_items;                // work items: (head, query tile) or (head, query block / pair)
   int n_static;               // sparse: items [0, n_static) run in the static order
+  // Single-pass search only: log2 of each row's mass in each key block,
+  // [B*H, nkb, L], and log2 e * LSE of each row, [B*H, L] (scratch), and the
+  // block masses W, [B*H, nkb, nkb].
+  float* ylog;
+  float* ylse2;
+  float* wmass;
 };
 
 struct MassParams {
@@ -82,6 +88,10 @@ hipError_t launch_block_mass(MassParams a, int head_dim, hipStream_t st);
 // (a: the attention's arguments with a.claim the optional work-queue
 // counters; m: the mass pass's, its lse unused).
 hipError_t launch_fused_search(AttnParams a, MassParams m, int head_dim, hipStream_t st);
+// Dense attention + LSE and the block masses of its LSE in one pass over
+// Q K^T (a.ylog, a.ylse2: scratch of B*H*nkb*L and B*H*L floats; a.wmass:
+// the masses), then the masses summed from the scratch.
+hipError_t launch_single_pass_search(AttnParams a, int head_dim, hipStream_t st);
 hipError_t launch_select(const SelectParams& p, hipStream_t st);
 
 }  // namespace adaspa
