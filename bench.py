@@ -371,11 +371,13 @@ def block64_record(q, k, v, lse, w, steps: int, dense_ms: float):
 
 
 def fused_search_record(q, k, v, w, steps: int):
-    """Algorithm 1 as one launch (adaspa_fused_online_search: dense attention
-    and LSE of 256 rows, then the masses of the same rows, then the
-    selection) against the same work as two calls (dense attention + LSE,
-    then the search from that LSE), coverage 0.9, at blocks 128 and 64; the
-    two are timed alternately on the same inputs and buffers."""
+    """Algorithm 1 three ways, coverage 0.9, at blocks 128 and 64: as two
+    calls (dense attention + LSE, then the search from that LSE), as one
+    launch of both passes (adaspa_fused_online_search) and with one pass over
+    Q K^T (adaspa_single_pass_online_search: the attention pass adds its own
+    exponentials per key block), beside dense attention alone; all four are
+    timed alternately on the same inputs and buffers.  The single pass's cost
+    over the dense pass is the search cost of the fresh-LSE step."""
     B, H, L, D = q.shape
     txt = {"text_start": w.text_start, "text_len": w.text_len}
     out = torch.empty_like(q)
@@ -388,18 +390,32 @@ def fused_search_record(q, k, v, w, steps: int):
         kw = dict(block=blk, mode="coverage", head_param_bp=tau, **txt)
         ws = torch.empty(ad.block_search_workspace(q.shape, blk, w.text_start, w.text_len, "coverage", tau),
                          dtype=torch.uint8, device="cuda")
+        wsp = torch.empty(ad.single_pass_online_search_workspace(q.shape, blk, w.text_start, w.text_len,
+                                                                 "coverage", tau),
+                          dtype=torch.uint8, device="cuda")
         r2 = ad.block_search(q, k, lse, workspace=ws, **kw)
         r1 = ad.block_search(q, k, lse, workspace=ws, **kw)
+        r3 = ad.block_search(q, k, lse, workspace=ws, **kw)
         tm = Timer()
         for it in range(1 + max(3, steps)):
             t = tm if it > 0 else Timer()
+            t("dense", ad.dense_attn_lse, q, k, v, out=out, lse=lse, workspace=dws)
             t("two_calls", lambda: (ad.dense_attn_lse(q, k, v, out=out, lse=lse, workspace=dws),
                                     ad.block_search(q, k, lse, workspace=ws, result=r2, **kw)))
             t("fused", ad.fused_online_search, q, k, v, out=out, lse=lse, workspace=ws, result=r1, **kw)
+            t("single_pass", ad.single_pass_online_search, q, k, v, out=out, lse=lse, workspace=wsp,
+              result=r3, **kw)
         ev = {n: float(np.mean(x)) for n, x in tm.collect().items()}
-        rec[f"block{blk}"] = {"fused_ms": round(ev["fused"], 3), "two_calls_ms": round(ev["two_calls"], 3),
-                              "fused_vs_two_calls": round(ev["fused"] / ev["two_calls"], 4)}
-        del ws, r1, r2
+        same = bool(torch.equal(r2.row_ptr, r3.row_ptr)) and bool(
+            torch.equal(r2.col_idx[:r2.nnz()], r3.col_idx[:r3.nnz()]))
+        rec[f"block{blk}"] = {"dense_ms": round(ev["dense"], 3), "two_calls_ms": round(ev["two_calls"], 3),
+                              "fused_ms": round(ev["fused"], 3), "single_pass_ms": round(ev["single_pass"], 3),
+                              "fused_vs_two_calls": round(ev["fused"] / ev["two_calls"], 4),
+                              "single_pass_vs_two_calls": round(ev["single_pass"] / ev["two_calls"], 4),
+                              "two_pass_search_vs_dense": round((ev["two_calls"] - ev["dense"]) / ev["dense"], 4),
+                              "single_pass_search_vs_dense": round((ev["single_pass"] - ev["dense"]) / ev["dense"], 4),
+                              "single_pass_pattern_equals_two_calls": same}
+        del ws, wsp, r1, r2, r3
     del out, lse, dws
     torch.cuda.empty_cache()
     return rec
@@ -526,10 +542,12 @@ def main():
                     help="sparse block size (the paper's default is 64; the 110K workload uses 128)")
     ap.add_argument("--no-amortised", action="store_true",
                     help="skip the 50-step denoising-loop workload")
-    ap.add_argument("--kernel", choices=["all", "dense", "sparse", "search", "fused", "copy", "gemm"],
+    ap.add_argument("--kernel", choices=["all", "dense", "sparse", "search", "fused", "single", "copy",
+                                         "gemm"],
                     default="all",
                     help="profile helper: run only one kernel in the timed loop ('fused': the "
-                         "fused online search, Algorithm 1 in one launch); 'copy' runs a "
+                         "fused online search, Algorithm 1 in one launch; 'single': the "
+                         "single-pass online search); 'copy' runs a "
                          "plain 1 GiB device copy, the reference for HBM byte counters; 'gemm' "
                          "times square bf16 library GEMMs (torch.matmul), a reference for the "
                          "chip's practical matrix throughput")
@@ -574,10 +592,17 @@ def main():
     sp_out = torch.empty_like(q)
     tau = [args.coverage_bp] * H
     wsb = ad.block_search_workspace((B, H, L, D), blk, w.text_start, w.text_len, "coverage", tau)
+    if args.kernel == "single":
+        wsb = ad.single_pass_online_search_workspace((B, H, L, D), blk, w.text_start, w.text_len, "coverage",
+                                                     tau)
     ws = torch.empty(wsb, dtype=torch.uint8, device="cuda")
     torch.cuda.synchronize()
 
     def step(t: Timer):
+        if args.kernel == "single":
+            return t("single", ad.single_pass_online_search, q, k, v, out=out, lse=lse, block=blk,
+                     text_start=w.text_start, text_len=w.text_len, mode="coverage", head_param_bp=tau,
+                     workspace=ws)
         if args.kernel == "fused":
             return t("fused", ad.fused_online_search, q, k, v, out=out, lse=lse, block=blk,
                      text_start=w.text_start, text_len=w.text_len, mode="coverage", head_param_bp=tau,
@@ -792,6 +817,9 @@ def main():
                    "step": "dense_attn_lse -> block_search -> block_sparse_attn"},
         "sparse_ms": round(sparse_ms, 3), "dense_ms": round(dense_ms, 3), "search_ms": round(search_ms, 3),
         "search_vs_dense": round(search_ms / dense_ms, 4),
+        # the fresh-LSE search (Algorithm 1) run with one pass over Q K^T: its
+        # cost on top of the dense pass that step runs anyway
+        "search_single_pass_vs_dense": (fused or {}).get(f"block{blk}", {}).get("single_pass_search_vs_dense"),
         "kernels": kernels, "density_sweep": sweep, "block64": b64, "head_adaptive": heads_cmp,
         "fused_online_search": fused,
         "amortised_loop": amort,

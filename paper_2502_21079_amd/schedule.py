@@ -33,15 +33,23 @@ import torch
 
 from . import (AdaspaError, SearchResult, block_search, block_search_workspace,
                block_sparse_attn, block_sparse_attn_workspace, dense_attn_lse,
-               dense_attn_workspace, fused_online_search)
+               dense_attn_workspace, fused_online_search, single_pass_online_search,
+               single_pass_online_search_workspace)
 
 __all__ = ["DENSE", "FUSED_SEARCH", "CACHED_SEARCH", "SPARSE", "SearchSchedule",
-           "AdaSpaAttention"]
+           "AdaSpaAttention", "SEARCH_KERNELS"]
 
 DENSE = "dense"                   # warm-up: full attention
 FUSED_SEARCH = "fused_search"     # Algorithm 1: full attention + LSE + search from the fresh LSE
 CACHED_SEARCH = "cached_search"   # Algorithm 2: search from the cached LSE, then sparse attention
 SPARSE = "sparse"                 # block-sparse attention with the current pattern
+
+# How the fused search step (Algorithm 1) runs: as one pass over Q K^T
+# (single_pass_online_search: the attention pass also adds its exponentials
+# per key block), as one launch of both passes (fused_online_search), or as
+# dense attention followed by the search.  All give the same output and LSE;
+# the masses agree to fp32 rounding.
+SEARCH_KERNELS = ("single_pass", "fused", "two_calls")
 
 
 @dataclass(frozen=True)
@@ -85,12 +93,14 @@ class AdaSpaAttention:
     ``step(t, q, k, v)`` makes the call the schedule names for step t and
     returns the attention output; the LSE of the fused search and the
     current block pattern persist between steps.  ``shape`` is (B, H, L, D);
-    the selection arguments are those of :func:`block_search`.  With
-    ``fused_kernel`` the fused search step runs Algorithm 1 as one launch
-    (:func:`fused_online_search`), otherwise as dense attention followed by
-    the search; the results are bitwise the same, and on MI355X the two
-    launches are the faster of the two (the fused kernel's mass pass runs at
-    the attention pass's two waves per SIMD instead of four)."""
+    the selection arguments are those of :func:`block_search`.
+    ``search_kernel`` (one of SEARCH_KERNELS) chooses how the fused search
+    step runs.  The default, "single_pass", takes one pass over Q K^T and is
+    the fastest on MI355X (110K tokens, block 128: about 0.1 of a dense pass
+    on top of it, against 0.55 for the two calls); it needs a workspace of
+    B*H*NB*L floats (9.1 GB at that size).  "fused" runs both passes in one
+    launch and "two_calls" dense attention followed by the search; those
+    two give bitwise the same results as each other."""
     shape: Tuple[int, int, int, int]
     block: int
     text_start: int
@@ -102,18 +112,26 @@ class AdaSpaAttention:
     schedule: SearchSchedule = field(default_factory=SearchSchedule)
     scale: Optional[float] = None
     device: str = "cuda"
-    fused_kernel: bool = False
+    search_kernel: str = "single_pass"
 
     def __post_init__(self):
+        if self.search_kernel not in SEARCH_KERNELS:
+            raise AdaspaError(f"search_kernel must be one of {SEARCH_KERNELS}, got {self.search_kernel!r}")
         B, H, L, D = self.shape
         dev = self.device
         self.lse = torch.empty(B, H, L, dtype=torch.float32, device=dev)   # the cached LSE
         self.search: Optional[SearchResult] = None                          # the current pattern
         self.search_step: Optional[int] = None
         self.lse_step: Optional[int] = None
-        self._ws_search = torch.empty(
-            block_search_workspace(self.shape, self.block, self.text_start, self.text_len, self.mode,
-                                   self.head_param_bp), dtype=torch.uint8, device=dev)
+        # The single pass's workspace holds the search's, so one buffer serves
+        # both searches.
+        wsb = block_search_workspace(self.shape, self.block, self.text_start, self.text_len, self.mode,
+                                     self.head_param_bp)
+        if self.search_kernel == "single_pass":
+            wsb = max(wsb, single_pass_online_search_workspace(
+                self.shape, self.block, self.text_start, self.text_len, self.mode, self.head_param_bp,
+                base_sparsity_bp=self.base_sparsity_bp, recall_threshold_bp=self.recall_threshold_bp))
+        self._ws_search = torch.empty(wsb, dtype=torch.uint8, device=dev)
         self._ws_dense = torch.empty(dense_attn_workspace(self.shape, self.scale), dtype=torch.uint8,
                                      device=dev)
         self._ws_sparse = torch.empty(block_sparse_attn_workspace(self.shape, self.block, self.scale),
@@ -138,8 +156,9 @@ class AdaSpaAttention:
                            workspace=self._ws_dense)
             return out, a
         if a == FUSED_SEARCH:
-            if self.fused_kernel:
-                _, _, self.search = fused_online_search(
+            if self.search_kernel in ("single_pass", "fused"):
+                fn = single_pass_online_search if self.search_kernel == "single_pass" else fused_online_search
+                _, _, self.search = fn(
                     q, k, v, block=self.block, text_start=self.text_start, text_len=self.text_len,
                     mode=self.mode, head_param_bp=self.head_param_bp, scale=self.scale, out=out,
                     lse=self.lse, workspace=self._ws_search, base_sparsity_bp=self.base_sparsity_bp,

@@ -269,6 +269,44 @@ def test_fused_search_rejects_bad_arguments(lib):
     assert call(prob=ctypes.byref(_prob(seqlen=0))) == 1
 
 
+def test_single_pass_search_rejects_bad_arguments(lib):
+    """The single-pass online search applies the fused search's checks; its
+    workspace adds B*H*NB*L floats of per-row block masses and B*H*L floats
+    of row LSEs to the search's, and a smaller one is refused before anything
+    is enqueued."""
+    p = _prob()
+    s, _a = _sel()
+    ws_search = lib.adaspa_block_search_workspace(ctypes.byref(p), ctypes.byref(s))
+    ws = lib.adaspa_single_pass_online_search_workspace(ctypes.byref(p), ctypes.byref(s))
+    nb = 2048 // 64
+    rnd = lambda x: (x + 255) // 256 * 256
+    assert ws == ws_search + rnd(2 * nb * 2048 * 4) + rnd(2 * 2048 * 4)
+    given, _b = _sel(flags=1 | 2)
+    assert lib.adaspa_single_pass_online_search_workspace(ctypes.byref(p), ctypes.byref(given)) == 0
+    assert lib.adaspa_single_pass_online_search_workspace(ctypes.byref(_prob(head_dim=96)),
+                                                          ctypes.byref(s)) == 0
+    cap = lib.adaspa_block_search_capacity(ctypes.byref(p), ctypes.byref(s))
+
+    def call(**o):
+        return lib.adaspa_single_pass_online_search(
+            o.get("prob", ctypes.byref(p)), o.get("q", FAKE), FAKE, o.get("v", FAKE), FAKE,
+            o.get("lse", None), o.get("sel", ctypes.byref(s)), FAKE, FAKE, FAKE, o.get("cap", cap),
+            None, None, o.get("ws", FAKE), o.get("wsb", ws), None)
+
+    assert call(v=None) == 1
+    assert call(q=ctypes.c_void_p(0x10008)) == 1
+    assert call(lse=ctypes.c_void_p(0x10002)) == 1
+    assert call(sel=None) == 1
+    assert call(sel=ctypes.byref(given)) == 1
+    assert call(cap=cap - 1) == 3
+    assert call(wsb=ws - 1) == 4
+    assert call(wsb=ws_search) == 4
+    assert call(ws=None) == 4
+    assert call(ws=ctypes.c_void_p(0x10010)) == 4
+    assert call(prob=ctypes.byref(_prob(head_dim=96))) == 2
+    assert call(prob=ctypes.byref(_prob(seqlen=0))) == 1
+
+
 def test_binding_checks_caller_outputs():
     """The binding refuses caller-provided outputs whose dtype, shape or
     layout differ from what the kernels write (the library sees pointers

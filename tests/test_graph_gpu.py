@@ -2,7 +2,8 @@
 validates its arguments and enqueues kernels (its work-queue counters are
 cleared by a kernel, not a memset), so one denoising step of the search
 schedule (dense attention + LSE, block search, block-sparse attention on the
-new pattern; or the fused online search, then block-sparse attention) can be
+new pattern; or the fused or single-pass online search, then block-sparse
+attention) can be
 captured once and replayed.  Between replays new seeded
 inputs are written into the captured buffers and the same step runs eagerly
 into separate buffers; every replay must equal the eager step bit for bit."""
@@ -22,20 +23,20 @@ CASES = {
 
 class Step:
     """One search step with every output and workspace allocated up front;
-    with ``fused`` the dense pass and the masses run as one launch (the fused
-    online search)."""
+    ``way`` runs the dense pass and the masses as two calls, as the fused
+    online search or as the single-pass online search."""
 
-    def __init__(self, w, q, k, v, fused=False):
+    def __init__(self, w, q, k, v, way="two_calls"):
         self.w, self.q, self.k, self.v = w, q, k, v
-        self.fused = fused
+        self.way = way
         B, H, L, D = q.shape
         self.kw = dict(block=w.block, text_start=w.text_start, text_len=w.text_len)
         self.tau = [9000] * H
         self.out_d = torch.empty_like(q)
         self.lse = torch.empty(B, H, L, dtype=torch.float32, device=q.device)
         self.ws_d = torch.empty(ad.dense_attn_workspace(q.shape), dtype=torch.uint8, device=q.device)
-        self.ws_s = torch.empty(ad.block_search_workspace(q.shape, w.block, w.text_start, w.text_len,
-                                                          "coverage", self.tau),
+        wsf = ad.single_pass_online_search_workspace if way == "single_pass" else ad.block_search_workspace
+        self.ws_s = torch.empty(wsf(q.shape, w.block, w.text_start, w.text_len, "coverage", self.tau),
                                 dtype=torch.uint8, device=q.device)
         self.ws_p = torch.empty(ad.block_sparse_attn_workspace(q.shape, w.block), dtype=torch.uint8,
                                 device=q.device)
@@ -44,10 +45,10 @@ class Step:
         self.res = None
 
     def __call__(self):
-        if self.fused:
-            _, _, self.res = ad.fused_online_search(self.q, self.k, self.v, mode="coverage",
-                                                    head_param_bp=self.tau, out=self.out_d, lse=self.lse,
-                                                    workspace=self.ws_s, result=self.res, **self.kw)
+        if self.way != "two_calls":
+            fn = ad.fused_online_search if self.way == "fused" else ad.single_pass_online_search
+            _, _, self.res = fn(self.q, self.k, self.v, mode="coverage", head_param_bp=self.tau,
+                                out=self.out_d, lse=self.lse, workspace=self.ws_s, result=self.res, **self.kw)
         else:
             ad.dense_attn_lse(self.q, self.k, self.v, out=self.out_d, lse=self.lse, workspace=self.ws_d)
             self.res = ad.block_search(self.q, self.k, self.lse, mode="coverage", head_param_bp=self.tau,
@@ -62,12 +63,12 @@ class Step:
                 "recall": self.res.head_recall, "sparse_out": self.out_s, "sparse_lse": self.lse_s}
 
 
-@pytest.mark.parametrize("fused", [False, True])
+@pytest.mark.parametrize("way", ["two_calls", "fused", "single_pass"])
 @pytest.mark.parametrize("case", sorted(CASES))
-def test_step_graph_replays_equal_eager(case, fused):
+def test_step_graph_replays_equal_eager(case, way):
     w = CASES[case]
     q, k, v = (t.contiguous() for t in make_qkv(w, device="cuda"))
-    cap = Step(w, q, k, v, fused)
+    cap = Step(w, q, k, v, way)
     side = torch.cuda.Stream()
     side.wait_stream(torch.cuda.current_stream())
     with torch.cuda.stream(side):
@@ -88,7 +89,7 @@ def test_step_graph_replays_equal_eager(case, fused):
         g.replay()
         torch.cuda.synchronize()
         got = {name: t.clone() for name, t in cap.outputs().items()}
-        ref = Step(w, qn.contiguous(), kn.contiguous(), vn.contiguous(), fused)
+        ref = Step(w, qn.contiguous(), kn.contiguous(), vn.contiguous(), way)
         ref()
         torch.cuda.synchronize()
         want = ref.outputs()

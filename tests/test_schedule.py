@@ -36,3 +36,12 @@ def test_no_warmup_and_single_search():
 def test_invalid_schedules(bad):
     with pytest.raises(AdaspaError):
         SearchSchedule(bad)
+
+
+def test_unknown_search_kernel_refused():
+    """The fused search step runs one of the three ways; any other name is
+    refused before anything is allocated."""
+    from paper_2502_21079_amd.schedule import SEARCH_KERNELS, AdaSpaAttention
+    assert SEARCH_KERNELS == ("single_pass", "fused", "two_calls")
+    with pytest.raises(AdaspaError, match="search_kernel"):
+        AdaSpaAttention((1, 2, 2048, 64), block=64, text_start=0, text_len=64, search_kernel="fast")

@@ -54,17 +54,17 @@ def _check_lists(res, sel, W, w):
     return same
 
 
-@pytest.mark.parametrize("fused_kernel", [False, True])
-def test_two_phase_schedule_against_oracle(fused_kernel):
-    """Both ways of running the fused search step: dense attention then the
-    search, or Algorithm 1 as one launch."""
+@pytest.mark.parametrize("search_kernel", ["single_pass", "fused", "two_calls"])
+def test_two_phase_schedule_against_oracle(search_kernel):
+    """Every way of running the fused search step: one pass over Q K^T, both
+    passes in one launch, or dense attention then the search."""
     w = TINY
     x0 = make_qkv(w, device="cuda", fp32=True)
     eps = make_drift_noise(w, device="cuda", seed=4)
     layer = AdaSpaAttention((w.batch, w.heads, w.seqlen, w.head_dim), block=w.block,
                             text_start=w.text_start, text_len=w.text_len, mode="topk",
                             head_param_bp=[KEEP] * w.heads, schedule=SearchSchedule((2, 5)),
-                            fused_kernel=fused_kernel)
+                            search_kernel=search_kernel)
     nb = w.nblocks
     lse2 = None            # the oracle's LSE of the fused-search step (per head)
     pattern = None         # the oracle's current pattern
