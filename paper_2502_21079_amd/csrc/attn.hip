@@ -1209,32 +1209,43 @@ __global__ __launch_bounds__(512, 1) void single_pass_search_kernel(AttnParams a
 }
 
 // W[bh][p][c] = sum over the rows i of query block p of
-// exp2(ylog[bh][c][i] - ylse2[bh][i]).  One workgroup per (query block, head);
-// each wave takes groups of 64 key blocks, reads each block's rows of p with
-// one lane per row (whole 256-byte runs), sums them over the wave in a fixed
-// order, and stores the group's 64 masses together.
-__global__ __launch_bounds__(256) void single_pass_reduce_kernel(AttnParams a) {
-  const int p = blockIdx.x, bh = blockIdx.y;
+// exp2(ylog[bh][c][i] - ylse2[bh][i]).  A workgroup of eight waves takes
+// eight consecutive query blocks of one head, one per wave; the waves walk
+// the key blocks in the same order, so for each key block the workgroup
+// reads one contiguous run of 8 x block rows (4 KB at block 128).  Each wave
+// reads its block's rows with one lane per row, BATCH key blocks at a time
+// with all their loads in flight together, sums them over the wave in a
+// fixed order, and stores 64 masses together.
+constexpr int kReduceWaves = 8;
+__global__ __launch_bounds__(64 * kReduceWaves) void single_pass_reduce_kernel(AttnParams a) {
+  const int bh = blockIdx.y;
   const int L = a.seqlen, nkb = a.nkb;
   const int lane = threadIdx.x & 63;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int p = blockIdx.x * kReduceWaves + wave;
+  if (p >= nkb) return;
   const int r0 = p * a.block;
   const int nr = L - r0 < a.block ? L - r0 : a.block;     // rows of this query block
   const bool v0 = lane < nr, v1 = lane + 64 < nr;         // this lane's rows r0 + lane, r0 + lane + 64
   const float* l2 = a.ylse2 + (size_t)bh * L + r0;
   const float m0 = v0 ? l2[lane] : 0.f, m1 = v1 ? l2[lane + 64] : 0.f;
   const float* y = a.ylog + (size_t)bh * nkb * L + r0 + lane;
-  for (int cg = wave * 64; cg < nkb; cg += 4 * 64) {
+  constexpr int BATCH = 16;                               // key blocks whose loads are in flight together
+  for (int cg = 0; cg < nkb; cg += 64) {
     const int n = nkb - cg < 64 ? nkb - cg : 64;
     float w_mine = 0.f;                                   // lane j keeps block cg + j
-#pragma unroll 8
-    for (int j = 0; j < 64; ++j) {
-      if (j < n) {
-        const float* yc = y + (size_t)(cg + j) * L;
-        float s = v0 ? fast_exp2(yc[0] - m0) : 0.f;
-        if (v1) s += fast_exp2(yc[64] - m1);
-        const float w = wave_sum(s);
-        w_mine = lane == j ? w : w_mine;
+    for (int j0 = 0; j0 < n; j0 += BATCH) {
+      float y0[BATCH], y1[BATCH];
+#pragma unroll
+      for (int u = 0; u < BATCH; ++u) {
+        const float* yc = y + (size_t)(cg + (j0 + u < n ? j0 + u : n - 1)) * L;
+        y0[u] = v0 ? yc[0] : -INFINITY;
+        y1[u] = v1 ? yc[64] : -INFINITY;
+      }
+#pragma unroll
+      for (int u = 0; u < BATCH; ++u) {
+        const float w = wave_sum(fast_exp2(y0[u] - m0) + fast_exp2(y1[u] - m1));
+        w_mine = lane == j0 + u ? w : w_mine;
       }
     }
     if (lane < n) a.wmass[((size_t)bh * nkb + p) * nkb + cg + lane] = w_mine;
@@ -1369,7 +1380,8 @@ hipError_t launch_single_pass_search(AttnParams a, int D, hipStream_t st) {
   else hipLaunchKernelGGL((single_pass_search_kernel<128>), dim3(a.n_wg), dim3(512), 0, st, a);
   const hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(single_pass_reduce_kernel, dim3(a.nkb, a.batch_heads), dim3(256), 0, st, a);
+  hipLaunchKernelGGL(single_pass_reduce_kernel, dim3((a.nkb + kReduceWaves - 1) / kReduceWaves, a.batch_heads),
+                     dim3(64 * kReduceWaves), 0, st, a);
   return hipGetLastError();
 }
 
