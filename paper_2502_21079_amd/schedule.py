@@ -100,7 +100,13 @@ class AdaSpaAttention:
     on top of it, against 0.55 for the two calls); it needs a workspace of
     B*H*NB*L floats (9.1 GB at that size).  "fused" runs both passes in one
     launch and "two_calls" dense attention followed by the search; those
-    two give bitwise the same results as each other."""
+    two give bitwise the same results as each other.
+
+    The search workspace is scratch (nothing in it is read by a later call),
+    so the layers of a model that run one after another can share one:
+    pass ``search_workspace`` (uint8, at least :meth:`search_workspace_bytes`
+    bytes, on the layer's device); otherwise each layer allocates its own.
+    The LSE and the pattern, which persist between steps, stay per layer."""
     shape: Tuple[int, int, int, int]
     block: int
     text_start: int
@@ -113,6 +119,17 @@ class AdaSpaAttention:
     scale: Optional[float] = None
     device: str = "cuda"
     search_kernel: str = "single_pass"
+    search_workspace: Optional[torch.Tensor] = None
+
+    def search_workspace_bytes(self) -> int:
+        """Bytes of scratch the searches of this layer need."""
+        wsb = block_search_workspace(self.shape, self.block, self.text_start, self.text_len, self.mode,
+                                     self.head_param_bp)
+        if self.search_kernel == "single_pass":
+            wsb = max(wsb, single_pass_online_search_workspace(
+                self.shape, self.block, self.text_start, self.text_len, self.mode, self.head_param_bp,
+                base_sparsity_bp=self.base_sparsity_bp, recall_threshold_bp=self.recall_threshold_bp))
+        return int(wsb)
 
     def __post_init__(self):
         if self.search_kernel not in SEARCH_KERNELS:
@@ -125,13 +142,15 @@ class AdaSpaAttention:
         self.lse_step: Optional[int] = None
         # The single pass's workspace holds the search's, so one buffer serves
         # both searches.
-        wsb = block_search_workspace(self.shape, self.block, self.text_start, self.text_len, self.mode,
-                                     self.head_param_bp)
-        if self.search_kernel == "single_pass":
-            wsb = max(wsb, single_pass_online_search_workspace(
-                self.shape, self.block, self.text_start, self.text_len, self.mode, self.head_param_bp,
-                base_sparsity_bp=self.base_sparsity_bp, recall_threshold_bp=self.recall_threshold_bp))
-        self._ws_search = torch.empty(wsb, dtype=torch.uint8, device=dev)
+        wsb = self.search_workspace_bytes()
+        ws = self.search_workspace
+        if ws is not None:
+            if ws.dtype != torch.uint8 or ws.numel() < wsb or ws.device != torch.device(dev) or \
+                    not ws.is_contiguous():
+                raise AdaspaError(f"search_workspace must be contiguous uint8 of at least {wsb} bytes on {dev}")
+            self._ws_search = ws
+        else:
+            self._ws_search = torch.empty(wsb, dtype=torch.uint8, device=dev)
         self._ws_dense = torch.empty(dense_attn_workspace(self.shape, self.scale), dtype=torch.uint8,
                                      device=dev)
         self._ws_sparse = torch.empty(block_sparse_attn_workspace(self.shape, self.block, self.scale),

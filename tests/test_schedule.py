@@ -45,3 +45,24 @@ def test_unknown_search_kernel_refused():
     assert SEARCH_KERNELS == ("single_pass", "fused", "two_calls")
     with pytest.raises(AdaspaError, match="search_kernel"):
         AdaSpaAttention((1, 2, 2048, 64), block=64, text_start=0, text_len=64, search_kernel="fast")
+
+
+def test_layers_share_one_search_workspace():
+    """The search workspace is scratch: layers can be given one shared
+    buffer of at least search_workspace_bytes(); a smaller or mistyped one is
+    refused.  (Built on the CPU device: only host-side sizes are computed.)"""
+    import torch
+    from paper_2502_21079_amd.schedule import AdaSpaAttention
+    kw = dict(shape=(1, 2, 2048, 64), block=64, text_start=0, text_len=64, head_param_bp=[9000, 9000],
+              device="cpu")
+    first = AdaSpaAttention(**kw)
+    need = first.search_workspace_bytes()
+    two = AdaSpaAttention(**kw, search_kernel="two_calls").search_workspace_bytes()
+    assert need > two > 0                     # the single pass adds its per-row block masses
+    ws = torch.empty(need, dtype=torch.uint8)
+    layers = [AdaSpaAttention(**kw, search_workspace=ws) for _ in range(3)]
+    assert all(layer._ws_search is ws for layer in layers)
+    assert len({id(layer.lse) for layer in layers}) == 3      # per-layer state stays separate
+    for bad in (ws[:need - 1], torch.empty(need, dtype=torch.int8)):
+        with pytest.raises(AdaspaError, match="search_workspace"):
+            AdaSpaAttention(**kw, search_workspace=bad)
