@@ -225,10 +225,12 @@ size_t adaspa_single_pass_online_search_workspace(const adaspa_problem* prob,
  * two-pass form needs is not taken.
  *   out, lse          bit for bit those of adaspa_dense_attn_lse (lse may be
  *                     NULL: the masses still use the fresh LSE)
- *   block_mass        the masses of the fresh LSE, equal to those of
- *                     adaspa_block_search up to fp32 rounding (a different
- *                     order of the same sums), within 1e-3 relative of the
- *                     exact values
+ *   block_mass        the masses of the fresh LSE, within 1e-3 relative of
+ *                     the exact values.  They are normalised by the LSE of
+ *                     the unrounded fp32 row sum; the stored lse normalises
+ *                     the bf16-rounded weights of the output, so
+ *                     adaspa_block_search given that lse returns masses
+ *                     that differ from these by up to 2^-9 relative
  *   row_ptr, col_idx, head_k, head_recall
  *                     the selection of those masses, as adaspa_block_search
  *                     (ADASPA_F_SCORES_GIVEN is not allowed:

@@ -383,8 +383,10 @@ def single_pass_online_search(q, k, v, *, block: int, text_start: int, text_len:
     """Algorithm 1 with one pass over Q K^T: dense attention with its LSE, the
     block masses of that LSE (added per key block from the attention pass's
     own exponentials) and the selection.  Returns (out, lse, SearchResult):
-    out and lse bit for bit those of :func:`dense_attn_lse`, the masses those
-    of :func:`block_search` up to fp32 rounding.  ``workspace`` (uint8 CUDA
+    out and lse bit for bit those of :func:`dense_attn_lse`; the masses are
+    normalised by the LSE of the unrounded row sum, so they differ from
+    :func:`block_search`'s given that lse (the LSE of the bf16-rounded
+    weights) by up to 2^-9 relative.  ``workspace`` (uint8 CUDA
     tensor of at least :func:`single_pass_online_search_workspace` bytes) is
     allocated here when not given."""
     _check_qkv(q, k, v)

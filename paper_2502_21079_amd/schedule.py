@@ -48,7 +48,8 @@ SPARSE = "sparse"                 # block-sparse attention with the current patt
 # (single_pass_online_search: the attention pass also adds its exponentials
 # per key block), as one launch of both passes (fused_online_search), or as
 # dense attention followed by the search.  All give the same output and LSE;
-# the masses agree to fp32 rounding.
+# the single pass's masses are normalised by the unrounded row sum, the
+# others' by the stored LSE, so they differ by up to 2^-9 relative.
 SEARCH_KERNELS = ("single_pass", "fused", "two_calls")
 
 

@@ -10,7 +10,9 @@ on sampled rows.
   attention on the selected pattern (Sec. 2.2, 4.1, 4.3) at the most key
   blocks a search takes (8,192), at block 128 (L just over one million
   tokens) and block 64 (the block-64 kernel's map of one row's key blocks is
-  then full), the last block ragged.
+  then full), the last block ragged; the single-pass search at the same
+  sizes (34 GB and 17 GB of per-row block masses): its output and LSE equal
+  to the dense kernel's, its masses against the oracle.
 """
 import numpy as np
 import pytest
@@ -109,6 +111,15 @@ def test_dense_search_sparse_at_most_blocks(block):
     tb = text_blocks(L, blk, w.text_start, w.text_len)
     kk = oracle.topk_count(50, nb, len(tb))
     assert kk == 41 and int(res.head_k[0, 0]) == kk
+    print(f"[max] {w.name}: single-pass search", flush=True)
+    o1, l1, r1 = ad.single_pass_online_search(q, k, v, block=blk, text_start=w.text_start,
+                                              text_len=w.text_len, mode="topk", head_param_bp=[50])
+    torch.cuda.synchronize()
+    assert torch.equal(o1, out) and torch.equal(l1, lse)
+    sp_sums = r1.block_mass[0, 0].double().sum(-1).cpu().numpy()
+    sp_mass = r1.block_mass[0, 0].cpu()              # checked against the oracle below
+    del o1, l1, r1
+    torch.cuda.empty_cache()
     print(f"[max] {w.name}: block-sparse attention on the selected pattern", flush=True)
     sp_out, sp_lse = ad.block_sparse_attn(q, k, v, res.row_ptr, res.col_idx, block=blk,
                                           text_start=w.text_start, text_len=w.text_len)
@@ -119,6 +130,7 @@ def test_dense_search_sparse_at_most_blocks(block):
     expect = np.full(nb, float(blk))
     expect[-1] = L - (nb - 1) * blk
     np.testing.assert_allclose(sums, expect, rtol=1e-3)
+    np.testing.assert_allclose(sp_sums, expect, rtol=1e-3)
 
     # dense output, LSE and masses of sampled query blocks against the oracle,
     # and block-sparse attention of those blocks over the keys they keep
@@ -135,6 +147,7 @@ def test_dense_search_sparse_at_most_blocks(block):
         check_lse(lse[0, 0, qi], l_ref, f"dense, query block {p}")
         m_ref = oracle.block_mass_rows(qh, kh, l_ref, w.scale, blk)
         check_mass(res.block_mass[0, 0, p], m_ref, f"masses, query block {p}")
+        check_mass(sp_mass[p], m_ref, f"single-pass masses, query block {p}")
         kr = _key_rows(ci[rpn[p]:rpn[p + 1]], blk, L)
         o_ref, l_ref = oracle.masked_attention(qh, kh[kr], vh[kr], np.ones(len(kr), bool), w.scale)
         check_out(sp_out[0, 0, qi], o_ref, f"sparse, query block {p}")

@@ -8,7 +8,7 @@ kernel's, so they must equal adaspa_dense_attn_lse's bit for bit.  Its block
 masses are the same fp32 sums as the two-pass search's in another order, so
 they are checked against the oracle's (within 1e-3 relative, every row at
 small sizes, sampled query blocks at larger ones) and against the two-pass
-search's.  The selection must equal the oracle's selection of the same fp32
+search's (within the bf16 rounding of the weights behind its LSE).  The selection must equal the oracle's selection of the same fp32
 masses bit for bit.  Shapes cover both block sizes and head dimensions,
 ragged lengths (a last block of 128 that holds one full tile and no ragged
 tile, a ragged tile after an odd and after an even number of full tiles),
@@ -71,13 +71,15 @@ def _oracle_masses(q, k, v, b, h, scale, block, blocks):
 def _check_against_two_pass(res, q, k, lse, w, mode, params):
     """The two-pass search from the stored LSE: the same sums in another fp32
     order, normalised by the LSE of the rounded weights instead of the
-    unrounded row sum."""
+    unrounded row sum.  Those two row sums differ by at most the weights'
+    bf16 rounding, 2^-9 of the sum, so the masses agree within that plus
+    fp32 noise."""
     two = ad.block_search(q, k, lse, block=w.block, text_start=w.text_start, text_len=w.text_len,
                           mode=mode, head_param_bp=params, base_sparsity_bp=9000)
     torch.cuda.synchronize()
     a, b = f64(res.block_mass), f64(two.block_mass)
     rel = np.abs(a - b) / (np.abs(b) + MASS_ABS_FLOOR)
-    assert rel.max() <= 1e-3, f"single pass against two-pass masses: max rel {rel.max():.3e}"
+    assert rel.max() <= 2 ** -9 + 2e-4, f"single pass against two-pass masses: max rel {rel.max():.3e}"
 
 
 @pytest.mark.parametrize("case", range(len(SHAPES)))
