@@ -167,3 +167,19 @@ def test_single_pass_long_sampled(block):
         check_mass(res.block_mass[0, h, blocks], ref, f"110K b{block} h{h}")
     sel = oracle.select_blocks(res.block_mass.cpu().numpy(), L, block, 0, w.text_len, "coverage", tau)
     _compare_selection(res, sel)
+
+
+def test_single_pass_without_lse_output():
+    """The LSE output is optional: the masses come from the kernel's own row
+    sums either way, so every output is the same bit for bit."""
+    w = TINY.replace(head_dim=128, block=128, seqlen=1000, patches=234)
+    q, k, v = make_qkv(w, device="cuda")
+    kw = dict(block=w.block, text_start=w.text_start, text_len=w.text_len, mode="coverage",
+              head_param_bp=[9000] * w.heads)
+    o1, l1, r1 = ad.single_pass_online_search(q, k, v, **kw)
+    o2, l2, r2 = ad.single_pass_online_search(q, k, v, want_lse=False, **kw)
+    torch.cuda.synchronize()
+    assert l2 is None and torch.equal(o1, o2)
+    assert torch.equal(r1.block_mass, r2.block_mass) and torch.equal(r1.row_ptr, r2.row_ptr)
+    n = r1.nnz()
+    assert torch.equal(r1.col_idx[:n], r2.col_idx[:n]) and torch.equal(r1.head_recall, r2.head_recall)
