@@ -485,12 +485,40 @@ def head_adaptive_comparison(steps: int, w=HETERO, s_bp: int = 9000, tau_bp: int
     return rec
 
 
+SWEEP_SCRATCH_CAP = 40 << 30     # bytes of single-pass scratch per call in the length sweep
+
+
+def single_pass_by_heads(q, k, v, **kw):
+    """The single-pass search over head groups whose scratch (B*H*NB*L
+    floats) stays under SWEEP_SCRATCH_CAP (one batch element: a head slice
+    is contiguous); returns the total HIP-event ms of the calls."""
+    B, H, L, D = q.shape
+    per_head = ad.single_pass_online_search_workspace((B, 1, L, D), kw["block"], kw["text_start"],
+                                                      kw["text_len"], kw["mode"], kw["head_param_bp"][:1])
+    g = max(1, min(H, SWEEP_SCRATCH_CAP // max(per_head, 1)))
+    ws = torch.empty(ad.single_pass_online_search_workspace((B, g, L, D), kw["block"], kw["text_start"],
+                                                           kw["text_len"], kw["mode"],
+                                                           kw["head_param_bp"][:g]),
+                     dtype=torch.uint8, device="cuda")
+    tm = Timer()
+    for h0 in range(0, H, g):
+        h1 = min(H, h0 + g)
+        args = dict(kw, head_param_bp=kw["head_param_bp"][h0:h1])
+        tm("sp", ad.single_pass_online_search, q[:, h0:h1], k[:, h0:h1], v[:, h0:h1], workspace=ws, **args)
+    ms = float(np.sum(tm.collect()["sp"]))
+    del ws
+    return ms, g
+
+
 def length_sweep(block: int, keep_bp: int = 1000, seconds=(4, 8, 12, 16, 24), reps: int = 2):
     """Attention-only scaling: dense vs. block-sparse attention across 720p
     clip lengths (4 latent frames per second of 3,440 patches, 256 text
     tokens, 24 heads, d = 128), at sparsity 0.9 (TOPK keep 10% with the text
     sink) chosen from the block masses of the fresh LSE.  Speedup = dense ms /
-    sparse ms; the search (mass + selection) is timed beside them."""
+    sparse ms; the two-pass search (mass + selection) is timed beside them,
+    and the single-pass search (dense attention, LSE and masses in one pass
+    over Q K^T, then the selection), whose cost over the dense pass is the
+    search cost of a fresh-LSE step."""
     rows = []
     for sec in seconds:
         w = LONG.replace(frames=4 * sec, seqlen=LONG.text_len + 4 * sec * LONG.patches, block=block,
@@ -513,13 +541,22 @@ def length_sweep(block: int, keep_bp: int = 1000, seconds=(4, 8, 12, 16, 24), re
         torch.cuda.synchronize()
         ev = {kname: float(np.mean(v_)) for kname, v_ in timer.collect().items()}
         nnz = res.nnz()
+        del res
+        spk = dict(block=block, mode="topk", head_param_bp=[keep_bp] * H, **txt)
+        single_pass_by_heads(q, k, v, **spk)                       # warm-up
+        sp_ms = [single_pass_by_heads(q, k, v, **spk) for _ in range(reps)]
+        sp, groups = float(np.mean([x[0] for x in sp_ms])), sp_ms[0][1]
+        sp_search = sp - ev["dense"]
         rows.append({"seconds": sec, "seq_len": L, "nblocks": w.nblocks, "dense_ms": round(ev["dense"], 3),
                      "search_ms": round(ev["search"], 3), "sparse_ms": round(ev["sparse"], 3),
                      "density": round(nnz / (B * H * w.nblocks ** 2), 5),
                      "sparse_tflops": round(sparse_flops(nnz, block, D) / (ev["sparse"] * 1e-3) / 1e12, 1),
                      "speedup_vs_dense": round(ev["dense"] / ev["sparse"], 3),
-                     "speedup_incl_search": round(ev["dense"] / (ev["sparse"] + ev["search"]), 3)})
-        del q, k, v, out, lse, res
+                     "speedup_incl_search": round(ev["dense"] / (ev["sparse"] + ev["search"]), 3),
+                     "single_pass_ms": round(sp, 3), "single_pass_heads_per_call": groups,
+                     "single_pass_search_ms": round(sp_search, 3),
+                     "speedup_incl_single_pass_search": round(ev["dense"] / (ev["sparse"] + sp_search), 3)})
+        del q, k, v, out, lse
         torch.cuda.empty_cache()
     return rows
 
