@@ -488,26 +488,22 @@ def head_adaptive_comparison(steps: int, w=HETERO, s_bp: int = 9000, tau_bp: int
 SWEEP_SCRATCH_CAP = 40 << 30     # bytes of single-pass scratch per call in the length sweep
 
 
-def single_pass_by_heads(q, k, v, **kw):
-    """The single-pass search over head groups whose scratch (B*H*NB*L
-    floats) stays under SWEEP_SCRATCH_CAP (one batch element: a head slice
-    is contiguous); returns the total HIP-event ms of the calls."""
-    B, H, L, D = q.shape
-    per_head = ad.single_pass_online_search_workspace((B, 1, L, D), kw["block"], kw["text_start"],
-                                                      kw["text_len"], kw["mode"], kw["head_param_bp"][:1])
-    g = max(1, min(H, SWEEP_SCRATCH_CAP // max(per_head, 1)))
-    ws = torch.empty(ad.single_pass_online_search_workspace((B, g, L, D), kw["block"], kw["text_start"],
-                                                           kw["text_len"], kw["mode"],
-                                                           kw["head_param_bp"][:g]),
-                     dtype=torch.uint8, device="cuda")
+def single_pass_capped(q, k, v, **kw):
+    """The single-pass search in one call with a workspace capped at
+    SWEEP_SCRATCH_CAP bytes: the library then runs the (batch, head) pairs in
+    groups whose per-row block masses fit; returns the HIP-event ms of the
+    call and the workspace bytes."""
+    shape = tuple(q.shape)
+    args = (kw["block"], kw["text_start"], kw["text_len"], kw["mode"], kw["head_param_bp"])
+    full = ad.single_pass_online_search_workspace(shape, *args)
+    least = ad.single_pass_online_search_min_workspace(shape, *args)
+    ws = torch.empty(max(least, min(full, SWEEP_SCRATCH_CAP)), dtype=torch.uint8, device="cuda")
     tm = Timer()
-    for h0 in range(0, H, g):
-        h1 = min(H, h0 + g)
-        args = dict(kw, head_param_bp=kw["head_param_bp"][h0:h1])
-        tm("sp", ad.single_pass_online_search, q[:, h0:h1], k[:, h0:h1], v[:, h0:h1], workspace=ws, **args)
+    tm("sp", ad.single_pass_online_search, q, k, v, workspace=ws, **kw)
     ms = float(np.sum(tm.collect()["sp"]))
+    n = ws.numel()
     del ws
-    return ms, g
+    return ms, n
 
 
 def length_sweep(block: int, keep_bp: int = 1000, seconds=(4, 8, 12, 16, 24), reps: int = 2):
@@ -543,9 +539,9 @@ def length_sweep(block: int, keep_bp: int = 1000, seconds=(4, 8, 12, 16, 24), re
         nnz = res.nnz()
         del res
         spk = dict(block=block, mode="topk", head_param_bp=[keep_bp] * H, **txt)
-        single_pass_by_heads(q, k, v, **spk)                       # warm-up
-        sp_ms = [single_pass_by_heads(q, k, v, **spk) for _ in range(reps)]
-        sp, groups = float(np.mean([x[0] for x in sp_ms])), sp_ms[0][1]
+        single_pass_capped(q, k, v, **spk)                         # warm-up
+        sp_ms = [single_pass_capped(q, k, v, **spk) for _ in range(reps)]
+        sp, ws_bytes = float(np.mean([x[0] for x in sp_ms])), sp_ms[0][1]
         sp_search = sp - ev["dense"]
         rows.append({"seconds": sec, "seq_len": L, "nblocks": w.nblocks, "dense_ms": round(ev["dense"], 3),
                      "search_ms": round(ev["search"], 3), "sparse_ms": round(ev["sparse"], 3),
@@ -553,7 +549,7 @@ def length_sweep(block: int, keep_bp: int = 1000, seconds=(4, 8, 12, 16, 24), re
                      "sparse_tflops": round(sparse_flops(nnz, block, D) / (ev["sparse"] * 1e-3) / 1e12, 1),
                      "speedup_vs_dense": round(ev["dense"] / ev["sparse"], 3),
                      "speedup_incl_search": round(ev["dense"] / (ev["sparse"] + ev["search"]), 3),
-                     "single_pass_ms": round(sp, 3), "single_pass_heads_per_call": groups,
+                     "single_pass_ms": round(sp, 3), "single_pass_workspace_gb": round(ws_bytes / 1e9, 2),
                      "single_pass_search_ms": round(sp_search, 3),
                      "speedup_incl_single_pass_search": round(ev["dense"] / (ev["sparse"] + sp_search), 3)})
         del q, k, v, out, lse

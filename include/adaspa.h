@@ -213,6 +213,17 @@ adaspa_status adaspa_fused_online_search(const adaspa_problem* prob, const void*
 size_t adaspa_single_pass_online_search_workspace(const adaspa_problem* prob,
                                                   const adaspa_select* sel);
 
+/* The least workspace adaspa_single_pass_online_search accepts: the
+ * search's workspace plus the per-row block masses and row LSEs of ONE
+ * (batch, head) pair (NB*L + L floats), each part rounded up to 256 bytes.
+ * Given less than adaspa_single_pass_online_search_workspace() but at least
+ * this, the call runs the attention pass over groups of as many (batch,
+ * head) pairs as fit, one after another, then the selection of all of them;
+ * the results are the same as with the full workspace.  0 for invalid
+ * arguments or ADASPA_F_SCORES_GIVEN. */
+size_t adaspa_single_pass_online_search_min_workspace(const adaspa_problem* prob,
+                                                      const adaspa_select* sel);
+
 /* Single-pass online search (Algorithm 1, Sec. 4.1-4.2, with one pass over
  * Q K^T): the outputs of adaspa_fused_online_search, computed differently.
  * The block mass W[p][c] is the sum over rows i of p of exp(s_ij - LSE_i)
@@ -235,11 +246,12 @@ size_t adaspa_single_pass_online_search_workspace(const adaspa_problem* prob,
  *                     the selection of those masses, as adaspa_block_search
  *                     (ADASPA_F_SCORES_GIVEN is not allowed:
  *                     ADASPA_ERR_INVALID_ARG)
- * workspace must hold adaspa_single_pass_online_search_workspace() bytes,
- * 256-byte aligned (ADASPA_ERR_WORKSPACE otherwise); it holds the
- * selection's scratch, the per-XCD work-queue counters (cleared by the call)
- * and the per-row block masses, and its contents need not be kept between
- * calls.  Capacity, alignment and the other errors as adaspa_block_search. */
+ * workspace must hold at least adaspa_single_pass_online_search_min_workspace()
+ * bytes, 256-byte aligned (ADASPA_ERR_WORKSPACE otherwise); with
+ * adaspa_single_pass_online_search_workspace() bytes every (batch, head)
+ * pair runs in one launch.  It holds the selection's scratch, the per-XCD
+ * work-queue counters (cleared by the call) and the per-row block masses,
+ * and its contents need not be kept between calls.  Capacity, alignment and the other errors as adaspa_block_search. */
 adaspa_status adaspa_single_pass_online_search(const adaspa_problem* prob, const void* q,
                                                const void* k, const void* v, void* out,
                                                float* lse, const adaspa_select* sel,

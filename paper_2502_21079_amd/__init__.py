@@ -29,7 +29,8 @@ __all__ = ["dense_attn_lse", "dense_attn_workspace", "block_search", "block_spar
            "block_sparse_attn_workspace", "block_sparse_attn_noalloc", "SearchResult",
            "library_path", "load_library", "AdaspaError", "EXPORTED_SYMBOLS",
            "block_search_workspace", "block_search_capacity", "fused_online_search",
-           "single_pass_online_search", "single_pass_online_search_workspace"]
+           "single_pass_online_search", "single_pass_online_search_workspace",
+           "single_pass_online_search_min_workspace"]
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
 _LIB_NAME = "libadaspa.so"
@@ -39,7 +40,7 @@ EXPORTED_SYMBOLS = ("adaspa_status_string", "adaspa_dense_attn_workspace", "adas
                     "adaspa_block_search", "adaspa_block_sparse_attn_workspace",
                     "adaspa_block_sparse_attn", "adaspa_block_sparse_attn_noalloc",
                     "adaspa_fused_online_search", "adaspa_single_pass_online_search_workspace",
-                    "adaspa_single_pass_online_search")
+                    "adaspa_single_pass_online_search_min_workspace", "adaspa_single_pass_online_search")
 
 SELECT_TOPK = 0
 SELECT_COVERAGE = 1
@@ -102,6 +103,8 @@ def load_library():
                                                ctypes.c_int64, i32p, f32p, vp, ctypes.c_size_t, vp]
     lib.adaspa_single_pass_online_search_workspace.restype = ctypes.c_size_t
     lib.adaspa_single_pass_online_search_workspace.argtypes = [P, S]
+    lib.adaspa_single_pass_online_search_min_workspace.restype = ctypes.c_size_t
+    lib.adaspa_single_pass_online_search_min_workspace.argtypes = [P, S]
     lib.adaspa_single_pass_online_search.restype = ctypes.c_int
     lib.adaspa_single_pass_online_search.argtypes = [P, vp, vp, vp, vp, f32p, S, f32p, i32p, i32p,
                                                      ctypes.c_int64, i32p, f32p, vp, ctypes.c_size_t, vp]
@@ -374,6 +377,20 @@ def single_pass_online_search_workspace(shape, block, text_start, text_len, mode
                                                                          ctypes.byref(sel)))
 
 
+def single_pass_online_search_min_workspace(shape, block, text_start, text_len, mode, head_param_bp=None,
+                                            text_sink=True, base_sparsity_bp: int = 8000,
+                                            recall_threshold_bp: int = 8000) -> int:
+    """The least workspace :func:`single_pass_online_search` accepts (one
+    (batch, head) pair's per-row block masses); with less than the full size
+    the call runs the (batch, head) pairs in groups, with the same results."""
+    B, H, L, D = shape
+    prob = _problem_shape(B, H, L, D, block, text_start, text_len, None)
+    sel, _keep = _select(mode, head_param_bp, text_sink, False, base_sparsity_bp, recall_threshold_bp,
+                         heads=H)
+    return int(load_library().adaspa_single_pass_online_search_min_workspace(ctypes.byref(prob),
+                                                                             ctypes.byref(sel)))
+
+
 def single_pass_online_search(q, k, v, *, block: int, text_start: int, text_len: int, mode: str,
                               head_param_bp: Optional[Sequence[int]] = None, text_sink: bool = True,
                               scale: Optional[float] = None, out=None, lse=None, want_lse: bool = True,
@@ -386,9 +403,11 @@ def single_pass_online_search(q, k, v, *, block: int, text_start: int, text_len:
     out and lse bit for bit those of :func:`dense_attn_lse`; the masses are
     normalised by the LSE of the unrounded row sum, so they differ from
     :func:`block_search`'s given that lse (the LSE of the bf16-rounded
-    weights) by up to 2^-9 relative.  ``workspace`` (uint8 CUDA
-    tensor of at least :func:`single_pass_online_search_workspace` bytes) is
-    allocated here when not given."""
+    weights) by up to 2^-9 relative.  ``workspace`` is a uint8 CUDA tensor:
+    with :func:`single_pass_online_search_workspace` bytes every (batch, head)
+    pair runs in one launch, with fewer (at least
+    :func:`single_pass_online_search_min_workspace`) in groups; when not given
+    (or below the minimum) the full size is allocated here."""
     _check_qkv(q, k, v)
     lib = load_library()
     B, H, L, D = q.shape
@@ -399,6 +418,7 @@ def single_pass_online_search(q, k, v, *, block: int, text_start: int, text_len:
                          recall_threshold_bp, heads=H)
     cap = lib.adaspa_block_search_capacity(ctypes.byref(prob), ctypes.byref(sel))
     wsb = lib.adaspa_single_pass_online_search_workspace(ctypes.byref(prob), ctypes.byref(sel))
+    wsb_min = lib.adaspa_single_pass_online_search_min_workspace(ctypes.byref(prob), ctypes.byref(sel))
     if cap < 0 or wsb == 0:
         _check(lib.adaspa_single_pass_online_search(ctypes.byref(prob), None, None, None, None, None,
                                                     ctypes.byref(sel), None, None, None, 0, None, None,
@@ -410,7 +430,7 @@ def single_pass_online_search(q, k, v, *, block: int, text_start: int, text_len:
     if lse is None and want_lse:
         lse = torch.empty(B, H, L, dtype=torch.float32, device=dev)
     res = _search_outputs(B, H, nb, cap, dev, result)
-    if workspace is None or workspace.numel() < wsb:
+    if workspace is None or workspace.numel() < wsb_min:
         workspace = torch.empty(int(wsb), dtype=torch.uint8, device=dev)
     _check(lib.adaspa_single_pass_online_search(ctypes.byref(prob), _ptr(q), _ptr(k), _ptr(v), _ptr(out),
                                                 _ptr(lse), ctypes.byref(sel), _ptr(res.block_mass),

@@ -375,12 +375,25 @@ adaspa_status adaspa_fused_online_search(const adaspa_problem* prob, const void*
   return enqueue_selection(prob, sel, block_mass, row_ptr, col_idx, head_k, head_recall, workspace, s);
 }
 
+// Bytes of the single pass's scratch for heads_per_call (batch, head) pairs
+// at a time: the per-row block masses and row LSEs of those pairs, after the
+// search's workspace (which the selection of all heads uses).
+static size_t single_pass_bytes(const adaspa_problem* prob, size_t heads_per_call) {
+  return workspace_layout(prob).total +
+         align_up(heads_per_call * (size_t)num_blocks(prob) * prob->seqlen * sizeof(float)) +
+         align_up(heads_per_call * (size_t)prob->seqlen * sizeof(float));
+}
+
 size_t adaspa_single_pass_online_search_workspace(const adaspa_problem* prob, const adaspa_select* sel) {
   if (check_problem(prob) != ADASPA_OK || check_select(prob, sel) != ADASPA_OK) return 0;
   if (sel->flags & ADASPA_F_SCORES_GIVEN) return 0;
-  const size_t bh = (size_t)prob->batch * prob->heads;
-  return workspace_layout(prob).total + align_up(bh * (size_t)num_blocks(prob) * prob->seqlen * sizeof(float)) +
-         align_up(bh * (size_t)prob->seqlen * sizeof(float));
+  return single_pass_bytes(prob, (size_t)prob->batch * prob->heads);
+}
+
+size_t adaspa_single_pass_online_search_min_workspace(const adaspa_problem* prob, const adaspa_select* sel) {
+  if (check_problem(prob) != ADASPA_OK || check_select(prob, sel) != ADASPA_OK) return 0;
+  if (sel->flags & ADASPA_F_SCORES_GIVEN) return 0;
+  return single_pass_bytes(prob, 1);
 }
 
 adaspa_status adaspa_single_pass_online_search(const adaspa_problem* prob, const void* q, const void* k,
@@ -401,31 +414,41 @@ adaspa_status adaspa_single_pass_online_search(const adaspa_problem* prob, const
     return ADASPA_ERR_INVALID_ARG;
   const int64_t need = adaspa_block_search_capacity(prob, sel);
   if (col_capacity < need) return ADASPA_ERR_CAPACITY;
-  const WsLayout wl = workspace_layout(prob);
-  if (!workspace || workspace_bytes < adaspa_single_pass_online_search_workspace(prob, sel) ||
-      ((uintptr_t)workspace % kAlign))
+  if (!workspace || workspace_bytes < single_pass_bytes(prob, 1) || ((uintptr_t)workspace % kAlign))
     return ADASPA_ERR_WORKSPACE;
+  // As many (batch, head) pairs per launch as the workspace holds: all of
+  // them with adaspa_single_pass_online_search_workspace() bytes.  Each pair
+  // is computed the same way whatever its group, so the results do not
+  // depend on the grouping.
+  const int bh_all = prob->batch * prob->heads;
+  int g = bh_all;
+  while (g > 1 && single_pass_bytes(prob, (size_t)g) > workspace_bytes) g = g / 2 > 1 ? g / 2 : 1;
+  while (g < bh_all && single_pass_bytes(prob, (size_t)g + 1) <= workspace_bytes) ++g;
 
   hipStream_t s = (hipStream_t)stream;
-  AttnParams a;
-  memset(&a, 0, sizeof a);
-  a.q = (const u16*)q;
-  a.k = (const u16*)k;
-  a.v = (const u16*)v;
-  a.o = (u16*)out;
-  a.lse = lse;
-  a.batch_heads = prob->batch * prob->heads;
-  a.seqlen = prob->seqlen;
-  a.block = prob->block;
-  a.nkb = num_blocks(prob);
-  a.scale = scale_of(prob);
-  a.scale_log2 = a.scale * 1.4426950408889634f;
-  a.claim = (uint32_t*)((char*)workspace + wl.claim);
-  a.ylog = (float*)((char*)workspace + wl.total);
-  a.ylse2 = (float*)((char*)workspace + wl.total +
-                     align_up((size_t)a.batch_heads * a.nkb * prob->seqlen * sizeof(float)));
-  a.wmass = block_mass;
-  if (launch_single_pass_search(a, prob->head_dim, s) != hipSuccess) return ADASPA_ERR_HIP;
+  const WsLayout wl = workspace_layout(prob);
+  const size_t L = (size_t)prob->seqlen, D = (size_t)prob->head_dim, nkb = (size_t)num_blocks(prob);
+  for (int g0 = 0; g0 < bh_all; g0 += g) {
+    const int gn = bh_all - g0 < g ? bh_all - g0 : g;
+    AttnParams a;
+    memset(&a, 0, sizeof a);
+    a.q = (const u16*)q + (size_t)g0 * L * D;
+    a.k = (const u16*)k + (size_t)g0 * L * D;
+    a.v = (const u16*)v + (size_t)g0 * L * D;
+    a.o = (u16*)out + (size_t)g0 * L * D;
+    a.lse = lse ? lse + (size_t)g0 * L : nullptr;
+    a.batch_heads = gn;
+    a.seqlen = prob->seqlen;
+    a.block = prob->block;
+    a.nkb = (int)nkb;
+    a.scale = scale_of(prob);
+    a.scale_log2 = a.scale * 1.4426950408889634f;
+    a.claim = (uint32_t*)((char*)workspace + wl.claim);
+    a.ylog = (float*)((char*)workspace + wl.total);
+    a.ylse2 = (float*)((char*)workspace + wl.total + align_up((size_t)gn * nkb * L * sizeof(float)));
+    a.wmass = block_mass + (size_t)g0 * nkb * nkb;
+    if (launch_single_pass_search(a, prob->head_dim, s) != hipSuccess) return ADASPA_ERR_HIP;
+  }
   return enqueue_selection(prob, sel, block_mass, row_ptr, col_idx, head_k, head_recall, workspace, s);
 }
 

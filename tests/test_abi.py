@@ -271,9 +271,10 @@ def test_fused_search_rejects_bad_arguments(lib):
 
 def test_single_pass_search_rejects_bad_arguments(lib):
     """The single-pass online search applies the fused search's checks; its
-    workspace adds B*H*NB*L floats of per-row block masses and B*H*L floats
-    of row LSEs to the search's, and a smaller one is refused before anything
-    is enqueued."""
+    full workspace adds B*H*NB*L floats of per-row block masses and B*H*L
+    floats of row LSEs to the search's, the least it accepts those of one
+    (batch, head) pair, and a smaller one is refused before anything is
+    enqueued."""
     p = _prob()
     s, _a = _sel()
     ws_search = lib.adaspa_block_search_workspace(ctypes.byref(p), ctypes.byref(s))
@@ -285,6 +286,10 @@ def test_single_pass_search_rejects_bad_arguments(lib):
     assert lib.adaspa_single_pass_online_search_workspace(ctypes.byref(p), ctypes.byref(given)) == 0
     assert lib.adaspa_single_pass_online_search_workspace(ctypes.byref(_prob(head_dim=96)),
                                                           ctypes.byref(s)) == 0
+    # the least accepted: one (batch, head) pair's scratch
+    least = lib.adaspa_single_pass_online_search_min_workspace(ctypes.byref(p), ctypes.byref(s))
+    assert least == ws_search + rnd(nb * 2048 * 4) + rnd(2048 * 4) and least < ws
+    assert lib.adaspa_single_pass_online_search_min_workspace(ctypes.byref(p), ctypes.byref(given)) == 0
     cap = lib.adaspa_block_search_capacity(ctypes.byref(p), ctypes.byref(s))
 
     def call(**o):
@@ -299,7 +304,7 @@ def test_single_pass_search_rejects_bad_arguments(lib):
     assert call(sel=None) == 1
     assert call(sel=ctypes.byref(given)) == 1
     assert call(cap=cap - 1) == 3
-    assert call(wsb=ws - 1) == 4
+    assert call(wsb=least - 1) == 4           # (any size from `least` up would be used)
     assert call(wsb=ws_search) == 4
     assert call(ws=None) == 4
     assert call(ws=ctypes.c_void_p(0x10010)) == 4

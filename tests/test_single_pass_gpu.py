@@ -183,3 +183,35 @@ def test_single_pass_without_lse_output():
     assert torch.equal(r1.block_mass, r2.block_mass) and torch.equal(r1.row_ptr, r2.row_ptr)
     n = r1.nnz()
     assert torch.equal(r1.col_idx[:n], r2.col_idx[:n]) and torch.equal(r1.head_recall, r2.head_recall)
+
+
+@pytest.mark.parametrize("mode", ["coverage", "hierarchical"])
+def test_single_pass_in_head_groups(mode):
+    """A workspace between the least and the full size runs the (batch, head)
+    pairs in groups: one pair at a time, four at a time (the last group
+    partial) and all at once give the same outputs bit for bit, also where
+    the selection ranks heads against each other (hierarchical)."""
+    w = TINY.replace(batch=2, heads=3, head_dim=128, block=64, seqlen=1000, patches=234)
+    q, k, v = make_qkv(w, device="cuda")
+    H = w.heads
+    params = None if mode == "hierarchical" else [9000, 8000, 7000]
+    kw = dict(block=w.block, text_start=w.text_start, text_len=w.text_len, mode=mode, head_param_bp=params,
+              base_sparsity_bp=9000)
+    shape = tuple(q.shape)
+    full = ad.single_pass_online_search_workspace(shape, w.block, w.text_start, w.text_len, mode, params,
+                                                  base_sparsity_bp=9000)
+    least = ad.single_pass_online_search_min_workspace(shape, w.block, w.text_start, w.text_len, mode, params,
+                                                       base_sparsity_bp=9000)
+    per_pair = (full - least) // 5                 # six pairs in full, one in the least
+    outs = []
+    for size in (least, least + 3 * per_pair, full):
+        ws = torch.empty(size, dtype=torch.uint8, device="cuda")
+        outs.append(ad.single_pass_online_search(q, k, v, workspace=ws, **kw))
+    torch.cuda.synchronize()
+    (o0, l0, r0) = outs[-1]
+    for o, l, r in outs[:-1]:
+        assert torch.equal(o, o0) and torch.equal(l, l0)
+        assert torch.equal(r.block_mass, r0.block_mass) and torch.equal(r.row_ptr, r0.row_ptr)
+        n = r0.nnz()
+        assert torch.equal(r.col_idx[:n], r0.col_idx[:n])
+        assert torch.equal(r.head_k, r0.head_k) and torch.equal(r.head_recall, r0.head_recall)
