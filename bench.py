@@ -485,7 +485,7 @@ def head_adaptive_comparison(steps: int, w=HETERO, s_bp: int = 9000, tau_bp: int
     return rec
 
 
-SWEEP_SCRATCH_CAP = 40 << 30     # bytes of single-pass scratch per call in the length sweep
+SWEEP_SCRATCH_CAP = 40 << 30     # bytes (40 GiB) of single-pass workspace in the length sweep
 
 
 def single_pass_capped(q, k, v, **kw):
