@@ -165,6 +165,15 @@ def _check_outputs(q, out, lse):
         raise AdaspaError(f"lse must be a contiguous fp32 [B, H, L] = {(B, H, L)} tensor on q's device")
 
 
+def _workspace_bytes(workspace, dev) -> int:
+    """Bytes of a caller's workspace tensor (any dtype), which must be a
+    contiguous tensor on the inputs' device: the library sees only its
+    pointer and size."""
+    if workspace.device != dev or not workspace.is_contiguous():
+        raise AdaspaError("workspace must be a contiguous tensor on q's device")
+    return workspace.numel() * workspace.element_size()
+
+
 def _select(mode: str, head_param_bp: Optional[Sequence[int]], text_sink: bool,
             scores_given: bool, base_sparsity_bp: int = 8000, recall_threshold_bp: int = 8000,
             heads: Optional[int] = None):
@@ -206,7 +215,7 @@ def dense_attn_lse(q, k, v, *, scale: Optional[float] = None, out=None, lse=None
         ws_bytes = int(lib.adaspa_dense_attn_workspace(ctypes.byref(prob)))
         if workspace is None:
             workspace = torch.empty(ws_bytes, dtype=torch.uint8, device=q.device)
-        ws_bytes = workspace.numel() * workspace.element_size()
+        ws_bytes = _workspace_bytes(workspace, q.device)
     else:
         workspace = None
     _check(lib.adaspa_dense_attn_lse(ctypes.byref(prob), _ptr(q), _ptr(k), _ptr(v), _ptr(out),
@@ -289,12 +298,12 @@ def block_search(q, k, lse, *, block: int, text_start: int, text_len: int,
                                        None, None, None, 0, None, None, None, 0, None))
         raise AdaspaError("invalid block_search arguments")
     res = _search_outputs(B, H, nb, cap, dev, result, scores)
-    if workspace is None or workspace.numel() < wsb:
+    if workspace is None or _workspace_bytes(workspace, dev) < wsb:
         workspace = torch.empty(int(wsb), dtype=torch.uint8, device=dev)
     _check(lib.adaspa_block_search(ctypes.byref(prob), _ptr(q), _ptr(k), _ptr(lse),
                                    ctypes.byref(sel), _ptr(res.block_mass), _ptr(res.row_ptr),
                                    _ptr(res.col_idx), int(res.col_idx.numel()), _ptr(res.head_k),
-                                   _ptr(res.head_recall), _ptr(workspace), int(workspace.numel()),
+                                   _ptr(res.head_recall), _ptr(workspace), _workspace_bytes(workspace, dev),
                                    _stream(dev)))
     return res
 
@@ -353,14 +362,14 @@ def fused_online_search(q, k, v, *, block: int, text_start: int, text_len: int, 
     if lse is None and want_lse:
         lse = torch.empty(B, H, L, dtype=torch.float32, device=dev)
     res = _search_outputs(B, H, nb, cap, dev, result)
-    if workspace is None or workspace.numel() < wsb:
+    if workspace is None or _workspace_bytes(workspace, dev) < wsb:
         workspace = torch.empty(int(wsb), dtype=torch.uint8, device=dev)
     _check(lib.adaspa_fused_online_search(ctypes.byref(prob), _ptr(q), _ptr(k), _ptr(v), _ptr(out),
                                           _ptr(lse), ctypes.byref(sel), _ptr(res.block_mass),
                                           _ptr(res.row_ptr), _ptr(res.col_idx),
                                           int(res.col_idx.numel()), _ptr(res.head_k),
                                           _ptr(res.head_recall), _ptr(workspace),
-                                          int(workspace.numel()), _stream(dev)))
+                                          _workspace_bytes(workspace, dev), _stream(dev)))
     return out, lse, res
 
 
@@ -430,14 +439,14 @@ def single_pass_online_search(q, k, v, *, block: int, text_start: int, text_len:
     if lse is None and want_lse:
         lse = torch.empty(B, H, L, dtype=torch.float32, device=dev)
     res = _search_outputs(B, H, nb, cap, dev, result)
-    if workspace is None or workspace.numel() < wsb_min:
+    if workspace is None or _workspace_bytes(workspace, dev) < wsb_min:
         workspace = torch.empty(int(wsb), dtype=torch.uint8, device=dev)
     _check(lib.adaspa_single_pass_online_search(ctypes.byref(prob), _ptr(q), _ptr(k), _ptr(v), _ptr(out),
                                                 _ptr(lse), ctypes.byref(sel), _ptr(res.block_mass),
                                                 _ptr(res.row_ptr), _ptr(res.col_idx),
                                                 int(res.col_idx.numel()), _ptr(res.head_k),
                                                 _ptr(res.head_recall), _ptr(workspace),
-                                                int(workspace.numel()), _stream(dev)))
+                                                _workspace_bytes(workspace, dev), _stream(dev)))
     return out, lse, res
 
 
@@ -472,7 +481,7 @@ def block_sparse_attn(q, k, v, row_ptr, col_idx, *, block: int, scale: Optional[
         ws_bytes = int(lib.adaspa_block_sparse_attn_workspace(ctypes.byref(prob)))
         if workspace is None:
             workspace = torch.empty(ws_bytes, dtype=torch.uint8, device=q.device)
-        ws_bytes = workspace.numel() * workspace.element_size()
+        ws_bytes = _workspace_bytes(workspace, q.device)
     else:
         workspace = None
     _check(lib.adaspa_block_sparse_attn(ctypes.byref(prob), _ptr(q), _ptr(k), _ptr(v),

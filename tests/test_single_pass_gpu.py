@@ -190,7 +190,8 @@ def test_single_pass_in_head_groups(mode):
     """A workspace between the least and the full size runs the (batch, head)
     pairs in groups: one pair at a time, four at a time (the last group
     partial) and all at once give the same outputs bit for bit, also where
-    the selection ranks heads against each other (hierarchical)."""
+    the selection ranks heads against each other (hierarchical).  A
+    workspace on another device is refused."""
     w = TINY.replace(batch=2, heads=3, head_dim=128, block=64, seqlen=1000, patches=234)
     q, k, v = make_qkv(w, device="cuda")
     H = w.heads
@@ -202,10 +203,18 @@ def test_single_pass_in_head_groups(mode):
                                                   base_sparsity_bp=9000)
     least = ad.single_pass_online_search_min_workspace(shape, w.block, w.text_start, w.text_len, mode, params,
                                                        base_sparsity_bp=9000)
-    per_pair = (full - least) // 5                 # six pairs in full, one in the least
+    # the search's workspace, then g pairs' per-row masses and row LSEs, each
+    # rounded up to 256 bytes
+    L, nb = w.seqlen, w.nblocks
+    rnd = lambda x: (x + 255) // 256 * 256
+    base = least - rnd(nb * L * 4) - rnd(L * 4)
+    assert full == base + rnd(6 * nb * L * 4) + rnd(6 * L * 4)
+    four = base + rnd(4 * nb * L * 4) + rnd(4 * L * 4)
     outs = []
-    for size in (least, least + 3 * per_pair, full):
-        ws = torch.empty(size, dtype=torch.uint8, device="cuda")
+    for size in (least, four, full):
+        # a workspace of any dtype counts in bytes: the middle one as int32
+        ws = (torch.empty(-(-size // 4), dtype=torch.int32, device="cuda") if size not in (least, full)
+              else torch.empty(size, dtype=torch.uint8, device="cuda"))
         outs.append(ad.single_pass_online_search(q, k, v, workspace=ws, **kw))
     torch.cuda.synchronize()
     (o0, l0, r0) = outs[-1]
@@ -215,3 +224,5 @@ def test_single_pass_in_head_groups(mode):
         n = r0.nnz()
         assert torch.equal(r.col_idx[:n], r0.col_idx[:n])
         assert torch.equal(r.head_k, r0.head_k) and torch.equal(r.head_recall, r0.head_recall)
+    with pytest.raises(ad.AdaspaError):
+        ad.single_pass_online_search(q, k, v, workspace=torch.empty(full, dtype=torch.uint8), **kw)
