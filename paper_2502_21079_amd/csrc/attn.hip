@@ -227,16 +227,37 @@ __device__ __forceinline__ void attn_fwd_body(AttnParams a, Tail&& tail) {
   float bsum = 0.f, rowf = 0.f;
   const int tsh = (BS && a.block == 128) ? 1 : 0;   // log2 of the tiles per key block
   const int tpb = 1 << tsh;
-  auto flush_block = [&](int c) {
+  // BS, pipelined tiles: the sum of a key block that ended at step t waits in
+  // bdone and is written in the middle of step t + 1, under its MFMAs, so
+  // the end of step t does not wait for that step's last additions, the
+  // exchange and the logarithm.  It is relative to the reference of step t,
+  // which moves again only after step t + 1's MFMAs.  cdone is its key
+  // block, -1 when none waits.
+  float bdone = 0.f;
+  int cdone = -1;
+  auto write_block = [&](float bs, int c) {
     if constexpr (BS) {
       float lo, hi;
-      half_pair(bsum, lo, hi);
+      half_pair(bs, lo, hi);
       const float b = lo + hi;
       // Column c of this head's [nkb, L] slab: a wave-uniform base, and the
       // row as a 32-bit offset.
       float* col = a.ylog + ((size_t)bh * a.nkb + (size_t)__builtin_amdgcn_readfirstlane(c)) * (size_t)L;
       if (hw == 0 && qrow < L) col[qrow] = (b > 0.f ? __builtin_amdgcn_logf(b) : -INFINITY) + ref.mc;
+    }
+  };
+  auto flush_block = [&](int c) {
+    if constexpr (BS) {
+      write_block(bsum, c);
       bsum = 0.f;
+    }
+  };
+  auto flush_waiting = [&]() {
+    if constexpr (BS) {
+      if (cdone >= 0) {
+        write_block(bdone, cdone);
+        cdone = -1;
+      }
     }
   };
   f32x16 o[ND];
@@ -330,10 +351,15 @@ __device__ __forceinline__ void attn_fwd_body(AttnParams a, Tail&& tail) {
         if (n >= PW || (n * SPAN) / PW != slot) return;
         ld.issue_n(n, fill, rKw, rVw, rMw, kbyte, vbyte, mbyte);
       };
+      auto hook = [&](int slot) {
+        loads(slot);
+        if constexpr (BS)
+          if (slot == (2 * NK + 4 * ND) / 2) flush_waiting();
+      };
       f32x16 s_next[2];
       bf16x8 p_cur[2][2];
       float tsum = 0.f;
-      pipelined_step<D, KS, VS, 2, BS>(loads, rdK + klane, rdV + voff, qf, s_cur, p_prev, s_next, p_cur, o,
+      pipelined_step<D, KS, VS, 2, BS>(hook, rdK + klane, rdV + voff, qf, s_cur, p_prev, s_next, p_cur, o,
                                        sl2, ref.mc, rsum, &tsum);
       move_reference<2, BS>(ref, rsum, bad, s_cur, p_cur, pend, pend_alpha, sl2, c32, false, &tsum);
       if constexpr (BS) {
@@ -343,7 +369,11 @@ __device__ __forceinline__ void attn_fwd_body(AttnParams a, Tail&& tail) {
         }
         bsum += tsum;
         rowf += tsum;
-        if (((t + 1) & (tpb - 1)) == 0) flush_block(t >> tsh);
+        if (((t + 1) & (tpb - 1)) == 0) {
+          bdone = bsum;
+          cdone = t >> tsh;
+          bsum = 0.f;
+        }
       }
 #pragma unroll
       for (int g = 0; g < 2; ++g) {
@@ -362,6 +392,7 @@ __device__ __forceinline__ void attn_fwd_body(AttnParams a, Tail&& tail) {
       step(t + 1, std::true_type{});
     }
     if (t < nf) step(t, std::true_type{});
+    flush_waiting();
     if (pend) {
 #pragma unroll
       for (int d = 0; d < ND; ++d)
