@@ -1028,11 +1028,22 @@ __device__ __forceinline__ void block_mass_body(const MassParams& a, int bh, int
   const int nrows = a.nkb - p0 < QB ? a.nkb - p0 : QB;      // rows of W this group owns
 
   float acc = 0.f;
-  auto finish_block = [&](int blk) {
-    const float w = wave_sum(acc);
+  auto reduce_block = [&](float v, int blk) {
+    const float w = wave_sum(v);
     if (lane == 0) sRed[blk & 1][wave] = w;
+  };
+  auto finish_block = [&](int blk) {
+    reduce_block(acc, blk);
     acc = 0.f;
   };
+  // Pipelined tiles: the sum of a key block that ended at step t waits in
+  // adone and is reduced over the wave in the middle of step t + 1, under
+  // its MFMAs, so the end of step t does not wait for that chain; it is
+  // published after step t + 1's barrier.  bdone is its block, -1 when none
+  // waits; npub counts the blocks published so far.
+  float adone = 0.f;
+  int bdone = -1;
+  int npub = 0;
   // After a barrier: waves combined in a fixed order (deterministic).
   auto publish = [&](int blk) {
     if (tid == 0) {
@@ -1090,16 +1101,28 @@ __device__ __forceinline__ void block_mass_body(const MassParams& a, int bh, int
         if (n >= NTOT || (n * NM) / NTOT != slot) return;
         ld.issue_n(n, fill, rKw, kbyte);
       };
+      auto hook = [&](int slot) {
+        loads(slot);
+        if (slot == NK && bdone >= 0) reduce_block(adone, bdone);
+      };
       f32x16 s_next[2];
-      mass_step<D, KS>(loads, rdK + klane, qf, s_cur, s_next, acc, sl2, nlse2);
+      mass_step<D, KS>(hook, rdK + klane, qf, s_cur, s_next, acc, sl2, nlse2);
       s_cur[0] = s_next[0];
       s_cur[1] = s_next[1];
-      const bool block_end = (t + 1) % sub == 0;
-      if (block_end) finish_block(t / sub);
+      const int reduced = bdone;
+      bdone = -1;
+      if ((t + 1) % sub == 0) {
+        adone = acc;
+        acc = 0.f;
+        bdone = t / sub;
+      }
       wait_vmem();
       __syncthreads();
-      flush(t / sub);               // blocks published before this barrier
-      if (block_end) publish(t / sub);
+      flush(npub);                  // blocks published before this barrier
+      if (reduced >= 0) {
+        publish(reduced);
+        npub = reduced + 1;
+      }
     };
     int t = 0;
     for (; t + 2 < nfull; t += 2) {
@@ -1109,6 +1132,13 @@ __device__ __forceinline__ void block_mass_body(const MassParams& a, int bh, int
     if (t + 1 < nfull) {
       step(t, sK1, sK0);
       ++t;
+    }
+    if (bdone >= 0) {
+      reduce_block(adone, bdone);
+      __syncthreads();
+      publish(bdone);
+      npub = bdone + 1;
+      bdone = -1;
     }
     // Last full tile: its scores are in s_cur.
 #pragma unroll

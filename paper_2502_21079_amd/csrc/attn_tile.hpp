@@ -56,13 +56,15 @@ __device__ __forceinline__ u32x4 rsrc_words(const void* base, uint32_t bytes) {
 // explicit instead: a loaded tile is read only after a vmcnt(0) wait and a
 // barrier, and a slot is refilled only after the barrier that follows its
 // last read.  M0 carries the LDS address; the compiler sets M0 itself before
-// each of its own uses, so clobbering it here is harmless.
+// each of its own uses, so clobbering it here is harmless.  The add that
+// forms M0 also sets SCC, which is declared clobbered too (a compare whose
+// result the compiler kept in SCC across the load would otherwise be lost).
 #pragma clang diagnostic push
 #pragma clang diagnostic ignored "-Winline-asm"
 template <int OFS>
 __device__ __forceinline__ void dma16(u32x4 rsrc, uint32_t lds, uint32_t voff, uint32_t soff) {
   asm volatile("s_add_u32 m0, %0, %4\n\ts_nop 0\n\tbuffer_load_dwordx4 %1, %2, %3 offen lds"
-               :: "s"(lds), "v"(voff), "s"(rsrc), "s"(soff), "n"(OFS) : "m0");
+               :: "s"(lds), "v"(voff), "s"(rsrc), "s"(soff), "n"(OFS) : "m0", "scc");
 }
 #pragma clang diagnostic pop
 
