@@ -359,7 +359,7 @@ __device__ __forceinline__ void attn_fwd_body(AttnParams a, Tail&& tail) {
       f32x16 s_next[2];
       bf16x8 p_cur[2][2];
       float tsum = 0.f;
-      pipelined_step<D, KS, VS, 2, BS>(hook, rdK + klane, rdV + voff, qf, s_cur, p_prev, s_next, p_cur, o,
+      pipelined_step<D, KS, VS, 2, BS, !SPARSE>(hook, rdK + klane, rdV + voff, qf, s_cur, p_prev, s_next, p_cur, o,
                                        sl2, ref.mc, rsum, &tsum);
       move_reference<2, BS>(ref, rsum, bad, s_cur, p_cur, pend, pend_alpha, sl2, c32, false, &tsum);
       if constexpr (BS) {

@@ -633,10 +633,14 @@ constexpr int kStageElems = NW * 32 * (D + 8);    // ring elements store_rows us
 // reference mc (below); a scheduling fence closes the slot, so the matrix
 // pipe and the VALU work side by side within the wave.  Four slots also add
 // the previous tile's rounded probabilities (the operands of its P V) to the
-// running row sums.
+// running row sums: the middle slot of each quarter of the step, or with
+// RS_FIRST its first slot, so the last of them is done well before the sum
+// test at the end of the step (dense attention: -1%; block-sparse
+// attention, whose loads and index picks crowd the first slots, keeps the
+// middle).  The sums are the same either way.
 // With BS, *tsum receives this lane's sum of the current tile's unrounded
 // exponentials, added pair by pair as the pairs are rounded.
-template <int D, int KS, int VS, int G = 2, bool BS = false, typename Hook>
+template <int D, int KS, int VS, int G = 2, bool BS = false, bool RS_FIRST = false, typename Hook>
 __device__ __forceinline__ void pipelined_step(Hook&& hook, const u16* klane, const u16* vlane,
                                                const bf16x8 (&qf)[D / 16], const f32x16 (&s_cur)[2],
                                                const bf16x8 (&p_prev)[2][2], f32x16 (&s_next)[2],
@@ -684,7 +688,8 @@ __device__ __forceinline__ void pipelined_step(Hook&& hook, const u16* klane, co
   // of the one just before it.  The last two slots' shares are finished after
   // the MFMAs.
   constexpr int PER = NS / NM;
-  constexpr int RSP = NM / (2 * G);           // row-sum MFMAs in slots RSP/2 + j*RSP
+  constexpr int RSP = NM / (2 * G);           // row-sum MFMAs in slots RS0 + j*RSP
+  constexpr int RS0 = RS_FIRST ? 0 : RSP / 2;
   float arg[NS], ex[NS];
   float fs = 0.f;
   auto stage_arg = [&](int i) {
@@ -726,7 +731,7 @@ __device__ __forceinline__ void pipelined_step(Hook&& hook, const u16* klane, co
   for (int i = 0; i < NM; ++i) {
     if (i + LA < NM) fetch(i + LA);
     mfma(i);
-    if (i % RSP == RSP / 2) rsum.add(p_prev[(i / RSP) >> 1][(i / RSP) & 1]);
+    if (i % RSP == RS0) rsum.add(p_prev[(i / RSP) >> 1][(i / RSP) & 1]);
     hook(i);
     stage_arg(i);
     if (i >= 1) stage_exp(i - 1);
