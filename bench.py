@@ -836,6 +836,19 @@ def main():
                        "frac": s20["frac_bf16_peak"], "traffic": measured_traffic("sparse"),
                        "target_frac": SPARSE_TARGET_FRAC,
                        "target_met": s20["frac_bf16_peak"] >= SPARSE_TARGET_FRAC}
+    # The single-pass search call (attention with its block sums, their
+    # reduction and the selection) against the MFMA work of the dense pass it
+    # contains: its time includes the reduction and the selection, so this
+    # understates the attention kernel's own rate.
+    roof_single = None
+    sp_rec = (fused or {}).get(f"block{blk}")
+    if sp_rec is not None:
+        sp_ms = sp_rec["single_pass_ms"]
+        t_sp, t_red = measured_traffic("single_pass"), measured_traffic("single_pass_reduce")
+        roof_single = {"kernel": "single_pass_online_search (call)", "bound": "mfma",
+                       "achieved": round(tf(f_dense, sp_ms), 1), "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
+                       "frac": round(tf(f_dense, sp_ms) / PEAK_BF16_TFLOPS, 4), "call_ms": sp_ms,
+                       "traffic": (t_sp + t_red) if (t_sp is not None and t_red is not None) else None}
     line = {
         "metric": "block-sparse attn ms + effective TFLOP/s @110K tok,24h,d128; search ms vs dense",
         "value": round(tf(f_sparse, sparse_ms), 2),
@@ -858,6 +871,7 @@ def main():
         "amortised_loop": amort,
         "two_phase_schedule": two_phase, "detail": detail,
         "roofline": roof, "roofline_sparse_keep20": roof_sparse, "roofline_block_mass": roof_mass,
+        "roofline_single_pass": roof_single,
         "cpu_baseline": cpu,
     }
     print(json.dumps(line), flush=True)
