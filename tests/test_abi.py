@@ -8,6 +8,7 @@ import os
 import re
 
 import pytest
+import torch
 
 import paper_2502_21079_amd as ad
 
@@ -329,3 +330,15 @@ def test_binding_checks_caller_outputs():
               torch.empty(2, 8, dtype=torch.float32)]:
         with pytest.raises(ad.AdaspaError, match="lse must"):
             ad._check_outputs(q, None, l)
+
+
+def test_workspace_tensors_count_in_bytes():
+    """A caller's workspace of any dtype counts in bytes; one on another
+    device than the inputs, or not contiguous, is refused before any call."""
+    cpu = torch.device("cpu")
+    assert ad._workspace_bytes(torch.empty(10, dtype=torch.int32), cpu) == 40
+    assert ad._workspace_bytes(torch.empty(7, dtype=torch.uint8), cpu) == 7
+    with pytest.raises(ad.AdaspaError):
+        ad._workspace_bytes(torch.empty(8, 2, dtype=torch.uint8).t(), cpu)
+    with pytest.raises(ad.AdaspaError):
+        ad._workspace_bytes(torch.empty(8, dtype=torch.uint8), torch.device("cuda", 0))
